@@ -1,0 +1,140 @@
+/*
+ * attn_jvp.h -- C ABI of the MI355X (gfx950) masked-attention forward + JVP library.
+ *
+ * Operation (paper App. B, "FlashAttention-2 JVP kernel with custom masks"):
+ *   O   = softmax(s * Q K^T + M) V                      (masked-attention equation)
+ *   dS  = s * (dQ K^T + Q dK^T), dS = 0 where M = -inf  (score-tangent equation;
+ *                                                        the mask has no tangent)
+ *   dO  = P dV + (P o (dS - rowsum(P o dS))) V          (tangent-output equation)
+ *   LSE = rowmax + ln(rowsum exp(S - rowmax))            (Algorithm 1, normalisation)
+ * computed in one fused online-softmax pass (Algorithm 1; epilogue equation
+ * dO = diag(l)^-1 (A + B - diag(r) O)).  M is the teacher-forcing chunk mask of
+ * autoregressive video diffusion (paper Sec. 3.1.1, packed [clean | noisy]
+ * forward): a clean query in chunk j sees clean chunks <= j; a noisy query in
+ * chunk i sees clean chunks < i and noisy chunk i.  Block-causal and full masks
+ * are the other two layouts of the same range-list representation (App. B,
+ * "Sparse custom-mask representation").
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Tensors are contiguous row-major [B, H, L, D] (batch, head, token, head_dim),
+ *   all with the same dtype (ATTN_DTYPE_*); LSE is fp32 [B, H, L].
+ * - Tensor pointers are DEVICE pointers; the chunk layout is a HOST struct whose
+ *   offsets array is HOST memory, read during the call only.
+ * - softmax_scale <= 0 selects s = 1/sqrt(D).
+ * - Work is enqueued on `stream` (a hipStream_t passed as void*, NULL = default
+ *   stream) and the call returns without synchronising: outputs are valid once
+ *   the stream has been synchronised.
+ * - The caller owns every buffer.  The library allocates no device memory and
+ *   keeps no per-call state, so calls are reentrant and may be captured in a
+ *   HIP graph.  Inputs are never written.  Outputs must not overlap inputs or
+ *   each other (checked by address range; overlap is ATTN_ERR_INVALID).
+ * - Return codes: ATTN_OK, or ATTN_ERR_INVALID (bad pointer, size or layout),
+ *   ATTN_ERR_UNSUPPORTED (dtype / head_dim not built), ATTN_ERR_HIP (a HIP
+ *   launch error).  All argument and layout validation happens before any HIP
+ *   call.  attn_last_error() returns a thread-local message for the last
+ *   nonzero return of this thread.  Nothing aborts or throws across the ABI.
+ * - Rows with no admissible key (impossible for the three built-in layouts)
+ *   produce O = 0, dO = 0, LSE = -inf.
+ */
+#ifndef ATTN_JVP_H
+#define ATTN_JVP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* element types of Q, K, V, dQ, dK, dV, O, dO */
+enum {
+  ATTN_DTYPE_F32 = 0,  /* fp32 in, fp32 math (exact-path kernel), fp32 out; D in {64, 128} */
+  ATTN_DTYPE_BF16 = 1  /* bf16 in, bf16 MFMA with fp32 accumulation, bf16 out; D in {64, 128} */
+};
+
+/* attention mask kinds (paper Sec. 3.1.1 and the background on TF / DF training) */
+enum {
+  ATTN_MASK_FULL = 0,             /* every query sees every key; num_chunks/offsets ignored */
+  ATTN_MASK_BLOCK_CAUSAL = 1,     /* query in chunk i sees chunks <= i; requires L == o_N */
+  ATTN_MASK_TEACHER_FORCING = 2   /* [clean c_1..c_N | noisy c_1..c_N]; requires L == 2 o_N */
+};
+
+enum {
+  ATTN_OK = 0,
+  ATTN_ERR_INVALID = 1,
+  ATTN_ERR_UNSUPPORTED = 2,
+  ATTN_ERR_HIP = 3
+};
+
+/* largest number of chunks a layout may have (the derived query-group table
+ * travels in the kernel arguments, so its size is bounded) */
+#define ATTN_MAX_CHUNKS 64
+
+/* Chunk layout of the mask.  chunk_offsets (HOST memory) holds num_chunks + 1
+ * strictly increasing prefix offsets 0 = o_0 < o_1 < ... < o_N of the chunk
+ * boundaries within ONE half of the TF sequence (teacher forcing) or within the
+ * sequence (block-causal).  Uniform chunks of C tokens use o_i = i * C. */
+typedef struct attn_chunk_layout {
+  int32_t kind;                  /* ATTN_MASK_* */
+  int32_t num_chunks;            /* N, 1..ATTN_MAX_CHUNKS (ignored for FULL) */
+  const int32_t* chunk_offsets;  /* N + 1 host ints (ignored for FULL, may be NULL) */
+} attn_chunk_layout;
+
+/* Fused masked attention forward + JVP (paper App. B, Algorithm 1).
+ *   in : Q, K, V, dQ, dK, dV  device [B, H, L, D], dtype `dtype`
+ *   out: O, dO                device [B, H, L, D], dtype `dtype`
+ *        LSE                  device fp32 [B, H, L], natural log, scaled-score domain
+ * B, H, L >= 1; D in {64, 128}. */
+int attn_jvp_fwd(int dtype, int B, int H, int L, int D,
+                 const void* Q, const void* K, const void* V,
+                 const void* dQ, const void* dK, const void* dV,
+                 const attn_chunk_layout* layout, float softmax_scale,
+                 void* O, void* dO, float* LSE, void* stream);
+
+/* Masked attention forward only (the primal part of Algorithm 1): O and LSE
+ * exactly as attn_jvp_fwd would produce them from the same Q, K, V. */
+int attn_fwd(int dtype, int B, int H, int L, int D,
+             const void* Q, const void* K, const void* V,
+             const attn_chunk_layout* layout, float softmax_scale,
+             void* O, float* LSE, void* stream);
+
+/* Host only.  Number of admissible (query, key) pairs of the layout over a
+ * sequence of L tokens, i.e. the pairs whose work is counted in throughput
+ * figures.  Returns -1 (and sets the error message) for an invalid layout. */
+int64_t attn_count_unmasked_pairs(const attn_chunk_layout* layout, int L);
+
+/* Host only.  Number of (query, key) pairs the bf16 kernel actually evaluates
+ * for this layout (whole key blocks, including masked lanes of partial blocks),
+ * for one (batch, head).  Returns -1 on an invalid layout or head_dim. */
+int64_t attn_count_computed_pairs(const attn_chunk_layout* layout, int L, int D);
+
+/* Host only.  The query-group / key-range table derived from the layout (paper
+ * App. B, "Sparse custom-mask representation": query interval [q0, q1) with a
+ * list of admissible key intervals; here at most two per group).  Writes
+ * 6 int32 per group: q0, q1, a0, a1, b0, b1 (key ranges [a0,a1) and [b0,b1),
+ * an empty range has begin == end) into `out` (capacity max_groups groups).
+ * Returns the number of groups, or -1 on an invalid layout or a too-small
+ * buffer. */
+int attn_query_groups(const attn_chunk_layout* layout, int L, int32_t* out, int max_groups);
+
+/* Host only.  Shape of the work decomposition of the bf16 kernels: query rows
+ * per work-group tile and keys per streamed key block. */
+void attn_tile_shape(int* rows_per_tile, int* keys_per_block);
+
+/* Host only.  Key-block plan of query tile `qtile` (rows [qtile*R, qtile*R + R)
+ * with R from attn_tile_shape) as the bf16 kernels execute it: the visited key
+ * block indices in visiting order go to blocks[], and full[i] = 1 if block i is
+ * admissible for every row of the tile (no per-row mask applied), else 0.
+ * Returns the number of visited blocks, or -1 on an invalid layout, tile index
+ * or a too-small buffer (capacity `cap`). */
+int attn_tile_plan(const attn_chunk_layout* layout, int L, int qtile,
+                   int32_t* blocks, int32_t* full, int cap);
+
+/* Thread-local description of the last nonzero return on this thread ("" if none). */
+const char* attn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ATTN_JVP_H */

@@ -1,0 +1,203 @@
+"""ctypes binding of libattnjvp.so (argument marshalling only).
+
+Every step of the computation runs in the HIP library.  Torch tensors supply
+device memory and the current HIP stream; outputs are allocated here with
+``torch.empty``.  There is no fallback: if the library is missing or a call
+fails, an exception is raised.
+"""
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+_LIBPATH = os.path.join(_PKG, "lib", "libattnjvp.so")
+
+DTYPE_F32, DTYPE_BF16 = 0, 1
+MASK_KINDS = {"full": 0, "block_causal": 1, "teacher_forcing": 2}
+MAX_CHUNKS = 64
+ERR_NAMES = {1: "invalid argument", 2: "unsupported", 3: "HIP error"}
+
+
+class AttnError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{ERR_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+class _Layout(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("num_chunks", ctypes.c_int32),
+                ("chunk_offsets", ctypes.POINTER(ctypes.c_int32))]
+
+
+_lib = None
+_vp = ctypes.c_void_p
+_i = ctypes.c_int
+
+
+def library_path():
+    return _LIBPATH
+
+
+def load_library():
+    """Load libattnjvp.so once; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIBPATH):
+        raise RuntimeError(f"HIP library not built: {_LIBPATH} is missing "
+                           "(run `python -m paper_2606_25473_amd.build`)")
+    lib = ctypes.CDLL(_LIBPATH)
+    lib.attn_jvp_fwd.argtypes = [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp,
+                                 ctypes.POINTER(_Layout), ctypes.c_float, _vp, _vp, _vp, _vp]
+    lib.attn_jvp_fwd.restype = _i
+    lib.attn_fwd.argtypes = [_i, _i, _i, _i, _i, _vp, _vp, _vp,
+                             ctypes.POINTER(_Layout), ctypes.c_float, _vp, _vp, _vp]
+    lib.attn_fwd.restype = _i
+    lib.attn_count_unmasked_pairs.argtypes = [ctypes.POINTER(_Layout), _i]
+    lib.attn_count_unmasked_pairs.restype = ctypes.c_int64
+    lib.attn_count_computed_pairs.argtypes = [ctypes.POINTER(_Layout), _i, _i]
+    lib.attn_count_computed_pairs.restype = ctypes.c_int64
+    lib.attn_query_groups.argtypes = [ctypes.POINTER(_Layout), _i, ctypes.POINTER(ctypes.c_int32), _i]
+    lib.attn_query_groups.restype = _i
+    lib.attn_tile_shape.argtypes = [ctypes.POINTER(_i), ctypes.POINTER(_i)]
+    lib.attn_tile_shape.restype = None
+    lib.attn_tile_plan.argtypes = [ctypes.POINTER(_Layout), _i, _i, ctypes.POINTER(ctypes.c_int32),
+                                   ctypes.POINTER(ctypes.c_int32), _i]
+    lib.attn_tile_plan.restype = _i
+    lib.attn_last_error.argtypes = []
+    lib.attn_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def make_layout(kind, offsets=None):
+    """C layout struct for mask ``kind`` ('full' | 'block_causal' | 'teacher_forcing' or its code)."""
+    code = MASK_KINDS[kind] if isinstance(kind, str) else int(kind)
+    offs = [] if offsets is None else [int(x) for x in offsets]
+    arr = (ctypes.c_int32 * max(1, len(offs)))(*offs) if offs else None
+    lay = _Layout(code, max(0, len(offs) - 1), arr if arr is not None else None)
+    lay._keep = arr  # keep the offsets array alive with the struct
+    return lay
+
+
+def last_error():
+    return load_library().attn_last_error().decode()
+
+
+def _check(rc):
+    if rc != 0:
+        raise AttnError(rc, last_error())
+
+
+def _dtype_code(t):
+    if t.dtype == torch.float32:
+        return DTYPE_F32
+    if t.dtype == torch.bfloat16:
+        return DTYPE_BF16
+    raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
+
+
+def _check_inputs(ts):
+    q = ts[0]
+    if q.dim() != 4:
+        raise ValueError("tensors must be [B, H, L, D]")
+    for t in ts:
+        if not t.is_cuda:
+            raise ValueError("tensors must live on a GPU")
+        if t.device != q.device or t.dtype != q.dtype or t.shape != q.shape:
+            raise ValueError("all inputs need the same device, dtype and shape")
+        if not t.is_contiguous():
+            raise ValueError("inputs must be contiguous")
+
+
+def attn_jvp_fwd(q, k, v, dq, dk, dv, kind="teacher_forcing", offsets=None, scale=None,
+                 out=None, stream=None):
+    """(O, dO, LSE) of masked softmax attention and its forward-mode tangent.
+
+    q..dv: contiguous [B, H, L, D] float32 or bfloat16 GPU tensors.  ``out`` may
+    supply preallocated (O, dO, LSE).  Work is queued on ``stream`` (default:
+    the current stream of q's device).
+    """
+    lib = load_library()
+    _check_inputs([q, k, v, dq, dk, dv])
+    B, H, L, D = q.shape
+    if out is None:
+        o, do = torch.empty_like(q), torch.empty_like(q)
+        lse = torch.empty((B, H, L), device=q.device, dtype=torch.float32)
+    else:
+        o, do, lse = out
+    lay = make_layout(kind, offsets)
+    st = stream if stream is not None else torch.cuda.current_stream(q.device)
+    with torch.cuda.device(q.device):
+        rc = lib.attn_jvp_fwd(_dtype_code(q), B, H, L, D, q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                              dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), ctypes.byref(lay),
+                              float(scale or 0.0), o.data_ptr(), do.data_ptr(), lse.data_ptr(),
+                              st.cuda_stream)
+    _check(rc)
+    return o, do, lse
+
+
+def attn_fwd(q, k, v, kind="teacher_forcing", offsets=None, scale=None, out=None, stream=None):
+    """(O, LSE) of masked softmax attention (forward only)."""
+    lib = load_library()
+    _check_inputs([q, k, v])
+    B, H, L, D = q.shape
+    if out is None:
+        o = torch.empty_like(q)
+        lse = torch.empty((B, H, L), device=q.device, dtype=torch.float32)
+    else:
+        o, lse = out
+    lay = make_layout(kind, offsets)
+    st = stream if stream is not None else torch.cuda.current_stream(q.device)
+    with torch.cuda.device(q.device):
+        rc = lib.attn_fwd(_dtype_code(q), B, H, L, D, q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                          ctypes.byref(lay), float(scale or 0.0), o.data_ptr(), lse.data_ptr(),
+                          st.cuda_stream)
+    _check(rc)
+    return o, lse
+
+
+def count_unmasked_pairs(kind, offsets, L):
+    """Admissible (query, key) pairs per (batch, head) (host-only library call)."""
+    n = load_library().attn_count_unmasked_pairs(ctypes.byref(make_layout(kind, offsets)), int(L))
+    if n < 0:
+        raise AttnError(1, last_error())
+    return int(n)
+
+
+def count_computed_pairs(kind, offsets, L, D=128):
+    """Pairs the bf16 kernel evaluates per (batch, head), masked lanes included."""
+    n = load_library().attn_count_computed_pairs(ctypes.byref(make_layout(kind, offsets)), int(L), int(D))
+    if n < 0:
+        raise AttnError(1, last_error())
+    return int(n)
+
+
+def query_groups(kind, offsets, L):
+    """Query-group table [(q0, q1, a0, a1, b0, b1), ...] derived by the library."""
+    cap = 2 * MAX_CHUNKS
+    buf = (ctypes.c_int32 * (6 * cap))()
+    n = load_library().attn_query_groups(ctypes.byref(make_layout(kind, offsets)), int(L), buf, cap)
+    if n < 0:
+        raise AttnError(1, last_error())
+    return [tuple(buf[6 * g:6 * g + 6]) for g in range(n)]
+
+
+def tile_shape():
+    """(query rows per tile, keys per block) of the bf16 kernels."""
+    r, k = _i(), _i()
+    load_library().attn_tile_shape(ctypes.byref(r), ctypes.byref(k))
+    return r.value, k.value
+
+
+def tile_plan(kind, offsets, L, qtile):
+    """[(key_block, is_full), ...] visited by query tile ``qtile`` of the bf16 kernels."""
+    cap = (int(L) + 31) // 32 + 8
+    blocks = (ctypes.c_int32 * cap)()
+    full = (ctypes.c_int32 * cap)()
+    n = load_library().attn_tile_plan(ctypes.byref(make_layout(kind, offsets)), int(L), int(qtile),
+                                      blocks, full, cap)
+    if n < 0:
+        raise AttnError(1, last_error())
+    return [(blocks[i], bool(full[i])) for i in range(n)]

@@ -1,0 +1,361 @@
+// attn_mfma.hip -- bf16 masked attention forward + JVP on gfx950 matrix cores.
+//
+// One work-group of 4 waves owns a query tile of 128 rows (32 per wave) of one
+// (batch, head) and streams the key blocks of its plan (schedule.hpp) through
+// LDS, 32 keys at a time, with the online-softmax recurrence of the paper's
+// Algorithm 1 (App. B): running max m, normaliser l, the primal accumulator O,
+// one fused tangent accumulator T = A + B (only their sum enters the
+// epilogue) and r = sum rowsum(P~ o dS).  Epilogue: O <- O / l,
+// LSE = m + ln l, dO = (T - r O) / l.
+//
+// Matrix-core formulation (v_mfma_f32_32x32x16_bf16, wave64).  Each wave
+// computes the TRANSPOSED score block S^T = K Q^T (32 keys x 32 queries) so that
+// a lane owns one query and 16 of the 32 keys:
+//   lane l -> query l%32, keys 8*(i/4) + 4*(l/32) + i%4 for accumulator slot i.
+// Row statistics then need one cross-lane step (lanes l and l^32), and the
+// probabilities P~^T feed the next contraction directly as the B operand,
+// provided the A operand (V^T, dV^T) lists keys in the same order.  V and dV
+// are stored key-major in LDS; the transposed operand comes from
+// ds_read_b64_tr_b16, which returns, in each 16-lane group, lane j <- element
+// j%4 of the 8-byte word addressed by lane 4e + j/4 (e = result element).
+//
+// Contractions per wave and 32-key block (D = 128, 32 MFMAs of 32x32x16 = 1 per
+// 16 keys x 32 d x 32 queries):
+//   S^T  = K Q^T                     8       (2D flop / pair)
+//   dS^T = dK Q^T + K dQ^T          16       (4D)
+//   O^T += V^T P~^T                  8       (2D)
+//   T^T += dV^T P~^T + V^T H~^T     16       (4D)      H~ = P~ o dS
+// = 12 D flop per (query, key) pair.
+//
+// Numerics: bf16 operands, fp32 accumulation; exp2 with log2(e) folded into the
+// score scale only (dS stays in natural units); P~ and H~ are rounded to bf16
+// (round-to-nearest-even) as MFMA operands while l and r accumulate the fp32
+// values.  The running max is refreshed lazily: the accumulators are rescaled
+// only when a row's block max exceeds the stored max by more than kLazy (in
+// log2 units), so P~ <= 2^kLazy; the result is the same function, since O, T, l
+// and r always share one reference max.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include "kernels.hpp"
+
+namespace attn {
+namespace {
+
+typedef __bf16 bf16_t;
+typedef bf16_t bf16x8 __attribute__((ext_vector_type(8)));
+typedef bf16_t bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int BR = kMfmaBr;
+constexpr int BC = kMfmaBc;
+constexpr int NTHREADS = 256;
+constexpr float kLazy = 8.0f;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+template <int D>
+struct Geo {
+  static constexpr int NCH = D / 8;               // 16-byte chunks per row
+  static constexpr int ROWB = D * 2;              // bytes per LDS row (bf16)
+  static constexpr int TILEB = BC * ROWB;         // bytes per LDS tile of BC keys
+  static constexpr int DT = D / 32;               // 32-wide d tiles of O^T / T^T
+  static constexpr int KS = D / 16;               // 16-deep k steps of the score contraction
+  static constexpr int CPT = BC * NCH;            // chunks per tile
+  static constexpr int CPTH = CPT / NTHREADS;     // chunks per thread per tile
+  static_assert(CPT % NTHREADS == 0, "tile must split evenly over the work-group");
+};
+
+// XOR swizzle of 16-byte chunks within an LDS row: conflict-free both for the
+// 16 consecutive rows of a b128 score-operand read and for the 4-row x 4-chunk
+// footprint of a transposed read.
+template <int D>
+__device__ __forceinline__ int swz(int row) {
+  return (((row & 3) << 2) | ((row >> 2) & 3)) & (Geo<D>::NCH - 1);
+}
+
+template <int D>
+__device__ __forceinline__ int lds_off(int row, int chunk) {
+  return row * Geo<D>::ROWB + ((chunk ^ swz<D>(row)) << 4);
+}
+
+__device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x4 ld_tr(const char* p) {
+  i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4*)(p));
+  return __builtin_bit_cast(bf16x4, v);
+}
+
+__device__ __forceinline__ bf16x8 cat(bf16x4 a, bf16x4 b) {
+  return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+
+__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32, 64); }
+
+template <int D, bool JVP>
+__global__ __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void attn_mfma_kernel(const AttnArgs a) {
+  using G = Geo<D>;
+  constexpr int NTILE = JVP ? 4 : 2;  // K, V (, dK, dV) per stage
+  constexpr int STAGEB = NTILE * G::TILEB;
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGEB];
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  const int lane = tid & 63;
+  const int hh = lane >> 5;   // which half of the wave (key sub-block within S^T)
+  const int L = a.L;
+
+  const int nqt = a.order.nt;
+  const int bh = blockIdx.x / nqt;
+  const int qtile = tile_of(a.order, blockIdx.x - bh * nqt);
+  const size_t head = (size_t)bh * L * D;
+  const bf16_t* __restrict__ Qg = (const bf16_t*)a.Q + head;
+  const bf16_t* __restrict__ Kg = (const bf16_t*)a.K + head;
+  const bf16_t* __restrict__ Vg = (const bf16_t*)a.V + head;
+  const bf16_t* __restrict__ dQg = (const bf16_t*)a.dQ + head;
+  const bf16_t* __restrict__ dKg = (const bf16_t*)a.dK + head;
+  const bf16_t* __restrict__ dVg = (const bf16_t*)a.dV + head;
+
+  const int q0 = qtile * BR;
+  const int q1 = q0 + BR < L ? q0 + BR : L;
+  const TilePlan plan = plan_tile(a.gt, q0, q1, BC);
+  const int nblk = plan_num_blocks(plan);
+
+  // ---- this lane's query row and its admissible key ranges
+  const int row = q0 + wave * 32 + (lane & 31);
+  int ra0 = 0, ra1 = 0, rb0 = 0, rb1 = 0;
+  for (int g = plan.g_first; g <= plan.g_last; ++g) {
+    if (row >= group_q_begin(a.gt, g) && row < a.gt.q_end[g]) {
+      ra0 = a.gt.a0[g]; ra1 = a.gt.a1[g]; rb0 = a.gt.b0[g]; rb1 = a.gt.b1[g];
+    }
+  }
+
+  // ---- Q^T / dQ^T as B operands: lane l holds row l%32, d = 16 s + 8 (l/32) + 0..7
+  bf16x8 qop[G::KS], dqop[JVP ? G::KS : 1];
+#pragma unroll
+  for (int s = 0; s < G::KS; ++s) {
+    if (row < L) {
+      qop[s] = *(const bf16x8*)(Qg + (size_t)row * D + 16 * s + 8 * hh);
+      if constexpr (JVP) dqop[s] = *(const bf16x8*)(dQg + (size_t)row * D + 16 * s + 8 * hh);
+    } else {
+      qop[s] = bf16x8{};
+      if constexpr (JVP) dqop[s] = bf16x8{};
+    }
+  }
+
+  // ---- global -> register -> LDS staging of one key block
+  u32x4 stg[NTILE][G::CPTH];
+  auto load_block = [&](int kb) {
+    const int k0 = kb * BC;
+#pragma unroll
+    for (int t = 0; t < NTILE; ++t) {
+      const bf16_t* src = t == 0 ? Kg : t == 1 ? Vg : t == 2 ? dKg : dVg;
+#pragma unroll
+      for (int j = 0; j < G::CPTH; ++j) {
+        const int cid = tid + NTHREADS * j;
+        const int r = cid / G::NCH, c = cid % G::NCH;
+        const int key = k0 + r;
+        stg[t][j] = key < L ? *(const u32x4*)(src + (size_t)key * D + c * 8) : u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+  };
+  auto store_block = [&](int st) {
+    char* base = smem + st * STAGEB;
+#pragma unroll
+    for (int t = 0; t < NTILE; ++t) {
+#pragma unroll
+      for (int j = 0; j < G::CPTH; ++j) {
+        const int cid = tid + NTHREADS * j;
+        const int r = cid / G::NCH, c = cid % G::NCH;
+        *(u32x4*)(base + t * G::TILEB + lds_off<D>(r, c)) = stg[t][j];
+      }
+    }
+  };
+
+  // per-lane LDS offsets of the transposed V / dV operand reads:
+  // tro[t][p][dt] for k step t (16 keys), key half p (+0 / +8), d tile dt
+  const int g16 = lane >> 4, s16 = lane & 15;
+  int tro[2][2][G::DT];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+      for (int dt = 0; dt < G::DT; ++dt) {
+        const int r = 16 * t + 8 * p + 4 * (g16 >> 1) + (s16 >> 2);
+        const int chunk = 4 * dt + 2 * (g16 & 1) + ((s16 & 3) >> 1);
+        tro[t][p][dt] = lds_off<D>(r, chunk) + 8 * (s16 & 1);
+      }
+
+  // ---- accumulators (O^T, T^T: lane holds query l%32, d = 32 dt + 8 (i/4) + 4 (l/32) + i%4)
+  f32x16 oacc[G::DT], tacc[JVP ? G::DT : 1];
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt) {
+    oacc[dt] = f32x16{};
+    if constexpr (JVP) tacc[dt] = f32x16{};
+  }
+  float m = -INFINITY;  // running reference max (log2 units); equal in lanes l and l^32
+  float lsum = 0.f;     // partial normaliser over this lane's keys
+  float rsum = 0.f;     // partial sum of P~ o dS over this lane's keys
+  const float c2 = a.scale * kLog2e;
+  const float sc = a.scale;
+
+  if (nblk > 0) {
+    load_block(plan_block(plan, 0));
+    store_block(0);
+  }
+  __syncthreads();
+
+  for (int it = 0; it < nblk; ++it) {
+    const int st = it & 1;
+    const bool more = it + 1 < nblk;
+    if (more) load_block(plan_block(plan, it + 1));
+
+    const int kb = plan_block(plan, it);
+    const int k0 = kb * BC;
+    const char* sK = smem + st * STAGEB;
+    const char* sV = sK + G::TILEB;
+    const char* sdK = sK + 2 * G::TILEB;
+    const char* sdV = sK + 3 * G::TILEB;
+
+    // ---- scores and score tangents (transposed): S^T = K Q^T, dS^T = dK Q^T + K dQ^T
+    f32x16 S = f32x16{}, dS = f32x16{};
+    const int krow = lane & 31;
+#pragma unroll
+    for (int s = 0; s < G::KS; ++s) {
+      const int off = lds_off<D>(krow, 2 * s + hh);
+      const bf16x8 kop = *(const bf16x8*)(sK + off);
+      S = mfma(kop, qop[s], S);
+      if constexpr (JVP) {
+        const bf16x8 dkop = *(const bf16x8*)(sdK + off);
+        dS = mfma(dkop, qop[s], dS);
+        dS = mfma(kop, dqop[s], dS);
+      }
+    }
+
+    // ---- mask (only on blocks not admissible for every row of the tile)
+    float s2[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s2[i] = S[i] * c2;
+    if (!block_is_full(plan, k0, BC, L)) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int key = k0 + 8 * (i >> 2) + 4 * hh + (i & 3);
+        const bool ok = key < L && ((key >= ra0 && key < ra1) || (key >= rb0 && key < rb1));
+        if (!ok) {
+          s2[i] = -INFINITY;
+          if constexpr (JVP) dS[i] = 0.f;
+        }
+      }
+    }
+
+    // ---- online softmax with lazy rescaling
+    float mx = s2[0];
+#pragma unroll
+    for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s2[i]);
+    mx = fmaxf(mx, xor32(mx));
+    const bool up = mx > m + kLazy;
+    if (__ballot(up)) {
+      const float mnew = up ? mx : m;
+      const float alpha = up ? __builtin_amdgcn_exp2f(m - mnew) : 1.f;
+      lsum *= alpha;
+      if constexpr (JVP) rsum *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < G::DT; ++dt) {
+        oacc[dt] *= alpha;
+        if constexpr (JVP) tacc[dt] *= alpha;
+      }
+      m = mnew;
+    }
+    const float mref = m == -INFINITY ? 0.f : m;
+    float p[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      p[i] = __builtin_amdgcn_exp2f(s2[i] - mref);
+      lsum += p[i];
+    }
+    float hv[16];
+    if constexpr (JVP) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        hv[i] = p[i] * (dS[i] * sc);
+        rsum += hv[i];
+      }
+    }
+
+    // ---- O^T += V^T P~^T ; T^T += dV^T P~^T + V^T H~^T
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      bf16x8 pb, hb;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        pb[j] = (bf16_t)p[8 * t + j];
+        if constexpr (JVP) hb[j] = (bf16_t)hv[8 * t + j];
+      }
+#pragma unroll
+      for (int dt = 0; dt < G::DT; ++dt) {
+        const bf16x8 vop = cat(ld_tr(sV + tro[t][0][dt]), ld_tr(sV + tro[t][1][dt]));
+        oacc[dt] = mfma(vop, pb, oacc[dt]);
+        if constexpr (JVP) {
+          const bf16x8 dvop = cat(ld_tr(sdV + tro[t][0][dt]), ld_tr(sdV + tro[t][1][dt]));
+          tacc[dt] = mfma(dvop, pb, tacc[dt]);
+          tacc[dt] = mfma(vop, hb, tacc[dt]);
+        }
+      }
+    }
+
+    if (more) store_block(st ^ 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue: combine the two half-waves' partial sums, normalise, store
+  const float l_tot = lsum + xor32(lsum);
+  const float r_tot = JVP ? rsum + xor32(rsum) : 0.f;
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  if (row < L) {
+    bf16_t* Og = (bf16_t*)a.O + head + (size_t)row * D;
+    bf16_t* dOg = (bf16_t*)a.dO + head + (size_t)row * D;
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int d = 32 * dt + 8 * q4 + 4 * hh;
+        bf16x4 ov, dov;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float on = oacc[dt][4 * q4 + e] * inv;
+          ov[e] = (bf16_t)on;
+          if constexpr (JVP) dov[e] = (bf16_t)((tacc[dt][4 * q4 + e] - r_tot * on) * inv);
+        }
+        *(bf16x4*)(Og + d) = ov;
+        if constexpr (JVP) *(bf16x4*)(dOg + d) = dov;
+      }
+    }
+    if (hh == 0)
+      a.LSE[(size_t)bh * L + row] = l_tot > 0.f ? (m + __log2f(l_tot)) * kLn2 : -INFINITY;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_mfma_bf16(const AttnArgs& a, int D, bool jvp, hipStream_t stream) {
+  const dim3 grid((unsigned)(a.order.nt * a.B * a.H));
+  const dim3 block(NTHREADS);
+  if (D == 128) {
+    if (jvp) hipLaunchKernelGGL((attn_mfma_kernel<128, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((attn_mfma_kernel<128, false>), grid, block, 0, stream, a);
+  } else {
+    if (jvp) hipLaunchKernelGGL((attn_mfma_kernel<64, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((attn_mfma_kernel<64, false>), grid, block, 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace attn

@@ -1,0 +1,108 @@
+// attn_simt.hip -- fp32 masked attention forward + JVP, exact-path kernel.
+//
+// The fp32 entry points must meet a much tighter tolerance than bf16 matrix
+// cores allow, so this kernel keeps every operand and product in fp32.  One
+// wave owns one query row; lanes split head_dim (1 or 2 elements per lane) and
+// the score and score tangent of each admissible key are reduced across the
+// wave.  Keys are visited one at a time over the row's own key ranges (exact
+// skipping), with the online recurrence of the paper's Algorithm 1 (App. B) at
+// a block size of one key: running max m, normaliser l, accumulators O,
+// T = A + B and r, epilogue O / l, LSE = m + ln l, dO = (T - r O) / l.
+#include <hip/hip_runtime.h>
+
+#include "kernels.hpp"
+
+namespace attn {
+namespace {
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+template <int D, bool JVP>
+__global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_simt_kernel(const AttnArgs a) {
+  constexpr int E = D / 64;  // elements per lane
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * kSimtRowsPerBlock + (threadIdx.x >> 6);
+  const int bh = blockIdx.y;
+  const int L = a.L;
+  if (row >= L) return;  // whole wave leaves; no barriers below
+
+  const size_t head = (size_t)bh * L * D;
+  const float* Q = (const float*)a.Q + head;
+  const float* K = (const float*)a.K + head;
+  const float* V = (const float*)a.V + head;
+  const float* dQ = (const float*)a.dQ + head;
+  const float* dK = (const float*)a.dK + head;
+  const float* dV = (const float*)a.dV + head;
+
+  const int g = find_group(a.gt, row);
+  const int rng[2][2] = {{a.gt.a0[g], a.gt.a1[g]}, {a.gt.b0[g], a.gt.b1[g]}};
+
+  float q[E], dq[E], o[E], t[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    q[e] = Q[(size_t)row * D + lane + 64 * e];
+    dq[e] = JVP ? dQ[(size_t)row * D + lane + 64 * e] : 0.f;
+    o[e] = 0.f;
+    t[e] = 0.f;
+  }
+  float m = -INFINITY, l = 0.f, r = 0.f;
+  const float sc = a.scale;
+
+  for (int ri = 0; ri < 2; ++ri) {
+    for (int k = rng[ri][0]; k < rng[ri][1]; ++k) {
+      float s = 0.f, ds = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const float kv = K[(size_t)k * D + lane + 64 * e];
+        s += q[e] * kv;
+        if (JVP) ds += dq[e] * kv + q[e] * dK[(size_t)k * D + lane + 64 * e];
+      }
+      s = wave_sum(s) * sc;
+      if (JVP) ds = wave_sum(ds) * sc;
+      const float mnew = fmaxf(m, s);
+      const float alpha = expf(m - mnew);  // m = -inf on the first key gives 0
+      const float p = expf(s - mnew);
+      l = l * alpha + p;
+      if (JVP) r = r * alpha + p * ds;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const float vv = V[(size_t)k * D + lane + 64 * e];
+        o[e] = o[e] * alpha + p * vv;
+        if (JVP) t[e] = t[e] * alpha + p * dV[(size_t)k * D + lane + 64 * e] + p * ds * vv;
+      }
+      m = mnew;
+    }
+  }
+
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  float* O = (float*)a.O + head + (size_t)row * D;
+  float* dO = JVP ? (float*)a.dO + head + (size_t)row * D : nullptr;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const float on = o[e] * inv;
+    O[lane + 64 * e] = on;
+    if (JVP) dO[lane + 64 * e] = (t[e] - r * on) * inv;
+  }
+  if (lane == 0) a.LSE[(size_t)bh * L + row] = l > 0.f ? m + logf(l) : -INFINITY;
+}
+
+}  // namespace
+
+hipError_t launch_simt_f32(const AttnArgs& a, int D, bool jvp, hipStream_t stream) {
+  const dim3 grid((unsigned)((a.L + kSimtRowsPerBlock - 1) / kSimtRowsPerBlock), (unsigned)(a.B * a.H));
+  const dim3 block(64 * kSimtRowsPerBlock);
+  if (D == 128) {
+    if (jvp) hipLaunchKernelGGL((attn_simt_kernel<128, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((attn_simt_kernel<128, false>), grid, block, 0, stream, a);
+  } else {
+    if (jvp) hipLaunchKernelGGL((attn_simt_kernel<64, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((attn_simt_kernel<64, false>), grid, block, 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace attn

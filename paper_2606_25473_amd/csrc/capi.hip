@@ -1,0 +1,179 @@
+// capi.hip -- the extern "C" entry points declared in include/attn_jvp.h.
+//
+// Every argument and the chunk layout are validated on the host before any
+// HIP call; the derived query-group table and tile order travel to the kernel
+// by value.  Errors are reported by return code plus a thread-local message.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+
+#include "attn_jvp.h"
+#include "kernels.hpp"
+#include "layout.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const std::string& msg) {
+  g_last_error = msg;
+  return code;
+}
+
+struct Span {
+  uintptr_t lo, hi;
+  const char* name;
+};
+
+bool overlap(const Span& x, const Span& y) { return x.lo < y.hi && y.lo < x.hi; }
+
+int elem_size(int dtype) { return dtype == ATTN_DTYPE_F32 ? 4 : dtype == ATTN_DTYPE_BF16 ? 2 : 0; }
+
+// Shared validation of attn_jvp_fwd / attn_fwd; fills the launch arguments.
+int prepare(bool jvp, int dtype, int B, int H, int L, int D, const void* Q, const void* K,
+            const void* V, const void* dQ, const void* dK, const void* dV,
+            const attn_chunk_layout* layout, float softmax_scale, void* O, void* dO, float* LSE,
+            attn::AttnArgs* args) {
+  if (dtype != ATTN_DTYPE_F32 && dtype != ATTN_DTYPE_BF16)
+    return fail(ATTN_ERR_UNSUPPORTED, "unsupported dtype " + std::to_string(dtype));
+  if (D != 64 && D != 128)
+    return fail(ATTN_ERR_UNSUPPORTED, "unsupported head_dim " + std::to_string(D) + " (built: 64, 128)");
+  if (B <= 0 || H <= 0 || L <= 0)
+    return fail(ATTN_ERR_INVALID, "B, H and L must be positive (B=" + std::to_string(B) +
+                                      ", H=" + std::to_string(H) + ", L=" + std::to_string(L) + ")");
+  if ((int64_t)B * H > (int64_t)1 << 20) return fail(ATTN_ERR_INVALID, "B * H too large");
+  if (!Q || !K || !V || !O || !LSE) return fail(ATTN_ERR_INVALID, "NULL tensor pointer");
+  if (jvp && (!dQ || !dK || !dV || !dO)) return fail(ATTN_ERR_INVALID, "NULL tangent pointer");
+  const int es = elem_size(dtype);
+  const uintptr_t tbytes = (uintptr_t)B * H * L * D * es;
+  const uintptr_t lbytes = (uintptr_t)B * H * L * sizeof(float);
+  const uintptr_t align = dtype == ATTN_DTYPE_BF16 ? 16 : 4;
+  const void* ins[6] = {Q, K, V, dQ, dK, dV};
+  const char* in_names[6] = {"Q", "K", "V", "dQ", "dK", "dV"};
+  for (int i = 0; i < (jvp ? 6 : 3); ++i)
+    if ((uintptr_t)ins[i] % align)
+      return fail(ATTN_ERR_INVALID, std::string(in_names[i]) + " is not " + std::to_string(align) +
+                                        "-byte aligned");
+  if ((uintptr_t)O % align || (jvp && (uintptr_t)dO % align) || (uintptr_t)LSE % 4)
+    return fail(ATTN_ERR_INVALID, "output pointer misaligned");
+  Span outs[3] = {{(uintptr_t)O, (uintptr_t)O + tbytes, "O"},
+                  {(uintptr_t)LSE, (uintptr_t)LSE + lbytes, "LSE"},
+                  {(uintptr_t)dO, (uintptr_t)dO + tbytes, "dO"}};
+  const int nout = jvp ? 3 : 2;
+  for (int i = 0; i < nout; ++i) {
+    for (int j = i + 1; j < nout; ++j)
+      if (overlap(outs[i], outs[j]))
+        return fail(ATTN_ERR_INVALID, std::string("outputs ") + outs[i].name + " and " + outs[j].name + " overlap");
+    for (int k = 0; k < (jvp ? 6 : 3); ++k) {
+      const Span in = {(uintptr_t)ins[k], (uintptr_t)ins[k] + tbytes, in_names[k]};
+      if (overlap(outs[i], in))
+        return fail(ATTN_ERR_INVALID, std::string("output ") + outs[i].name + " overlaps input " + in.name);
+    }
+  }
+  std::string err;
+  if (!attn::build_groups(layout, L, &args->gt, &err)) return fail(ATTN_ERR_INVALID, err);
+  args->Q = Q; args->K = K; args->V = V;
+  args->dQ = dQ; args->dK = dK; args->dV = dV;
+  args->O = O; args->dO = dO; args->LSE = LSE;
+  args->B = B; args->H = H; args->L = L;
+  args->scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)D);
+  args->order = attn::make_tile_order(layout, L, attn::kMfmaBr);
+  return ATTN_OK;
+}
+
+int launch(bool jvp, int dtype, int D, const attn::AttnArgs& args, void* stream) {
+  const hipError_t e = dtype == ATTN_DTYPE_BF16
+                           ? attn::launch_mfma_bf16(args, D, jvp, (hipStream_t)stream)
+                           : attn::launch_simt_f32(args, D, jvp, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(ATTN_ERR_HIP, std::string("HIP launch failed: ") + hipGetErrorString(e));
+  return ATTN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int attn_jvp_fwd(int dtype, int B, int H, int L, int D, const void* Q, const void* K, const void* V,
+                 const void* dQ, const void* dK, const void* dV, const attn_chunk_layout* layout,
+                 float softmax_scale, void* O, void* dO, float* LSE, void* stream) {
+  attn::AttnArgs args;
+  const int rc = prepare(true, dtype, B, H, L, D, Q, K, V, dQ, dK, dV, layout, softmax_scale, O, dO, LSE, &args);
+  if (rc != ATTN_OK) return rc;
+  return launch(true, dtype, D, args, stream);
+}
+
+int attn_fwd(int dtype, int B, int H, int L, int D, const void* Q, const void* K, const void* V,
+             const attn_chunk_layout* layout, float softmax_scale, void* O, float* LSE, void* stream) {
+  attn::AttnArgs args;
+  const int rc = prepare(false, dtype, B, H, L, D, Q, K, V, nullptr, nullptr, nullptr, layout, softmax_scale,
+                         O, nullptr, LSE, &args);
+  if (rc != ATTN_OK) return rc;
+  return launch(false, dtype, D, args, stream);
+}
+
+int64_t attn_count_unmasked_pairs(const attn_chunk_layout* layout, int L) {
+  attn::GroupTable gt;
+  std::string err;
+  if (!attn::build_groups(layout, L, &gt, &err)) {
+    fail(ATTN_ERR_INVALID, err);
+    return -1;
+  }
+  return attn::count_pairs(gt);
+}
+
+int64_t attn_count_computed_pairs(const attn_chunk_layout* layout, int L, int D) {
+  if (D != 64 && D != 128) {
+    fail(ATTN_ERR_UNSUPPORTED, "unsupported head_dim " + std::to_string(D));
+    return -1;
+  }
+  attn::GroupTable gt;
+  std::string err;
+  if (!attn::build_groups(layout, L, &gt, &err)) {
+    fail(ATTN_ERR_INVALID, err);
+    return -1;
+  }
+  return attn::count_computed_pairs(gt, L, attn::kMfmaBr, attn::kMfmaBc);
+}
+
+int attn_query_groups(const attn_chunk_layout* layout, int L, int32_t* out, int max_groups) {
+  attn::GroupTable gt;
+  std::string err;
+  if (!attn::build_groups(layout, L, &gt, &err)) return fail(ATTN_ERR_INVALID, err), -1;
+  if (!out || max_groups < gt.n) return fail(ATTN_ERR_INVALID, "output buffer too small"), -1;
+  for (int g = 0; g < gt.n; ++g) {
+    int32_t* r = out + 6 * g;
+    r[0] = attn::group_q_begin(gt, g);
+    r[1] = gt.q_end[g];
+    r[2] = gt.a0[g]; r[3] = gt.a1[g];
+    r[4] = gt.b0[g]; r[5] = gt.b1[g];
+  }
+  return gt.n;
+}
+
+void attn_tile_shape(int* rows_per_tile, int* keys_per_block) {
+  if (rows_per_tile) *rows_per_tile = attn::kMfmaBr;
+  if (keys_per_block) *keys_per_block = attn::kMfmaBc;
+}
+
+int attn_tile_plan(const attn_chunk_layout* layout, int L, int qtile, int32_t* blocks, int32_t* full, int cap) {
+  attn::GroupTable gt;
+  std::string err;
+  if (!attn::build_groups(layout, L, &gt, &err)) return fail(ATTN_ERR_INVALID, err), -1;
+  const int br = attn::kMfmaBr, bc = attn::kMfmaBc;
+  if (qtile < 0 || (int64_t)qtile * br >= L) return fail(ATTN_ERR_INVALID, "query tile out of range"), -1;
+  const int q0 = qtile * br;
+  const int q1 = q0 + br < L ? q0 + br : L;
+  const attn::TilePlan p = attn::plan_tile(gt, q0, q1, bc);
+  const int nb = attn::plan_num_blocks(p);
+  if (!blocks || !full || cap < nb) return fail(ATTN_ERR_INVALID, "output buffer too small"), -1;
+  for (int i = 0; i < nb; ++i) {
+    blocks[i] = attn::plan_block(p, i);
+    full[i] = attn::block_is_full(p, blocks[i] * bc, bc, L) ? 1 : 0;
+  }
+  return nb;
+}
+
+const char* attn_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

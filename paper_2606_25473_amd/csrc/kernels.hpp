@@ -1,0 +1,38 @@
+// kernels.hpp -- kernel launch interface used by the C ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "schedule.hpp"
+
+namespace attn {
+
+// Arguments of one attention launch.  Everything the kernels need travels by
+// value in the kernel arguments: the library holds no device memory.
+struct AttnArgs {
+  const void* Q;
+  const void* K;
+  const void* V;
+  const void* dQ;   // tangents: unused by the forward-only kernels
+  const void* dK;
+  const void* dV;
+  void* O;
+  void* dO;
+  float* LSE;
+  int B, H, L;
+  float scale;      // softmax scale s applied to scores and score tangents
+  GroupTable gt;
+  TileOrder order;
+};
+
+// bf16 MFMA kernels: query tiles of kMfmaBr rows (4 waves x 32 rows), key blocks of kMfmaBc keys.
+constexpr int kMfmaBr = 128;
+constexpr int kMfmaBc = 32;
+
+// fp32 exact-path kernels: one wave per query row.
+constexpr int kSimtRowsPerBlock = 4;
+
+hipError_t launch_mfma_bf16(const AttnArgs& a, int D, bool jvp, hipStream_t stream);
+hipError_t launch_simt_f32(const AttnArgs& a, int D, bool jvp, hipStream_t stream);
+
+}  // namespace attn

@@ -1,0 +1,208 @@
+"""GPU parity of the HIP path against the fp64 CPU oracle (marked ``gpu``).
+
+Small and edge-case shapes are compared element by element over every output;
+the full Wan-shaped workloads are run in the launch configuration the bench
+times and compared on sampled rows (chunk and tile boundaries plus seeded
+random rows), which the oracle evaluates one by one.
+
+Tolerance: relative L2 error ||x - x_ref|| / ||x_ref|| per output (O, dO, LSE),
+<= 1e-2 for bf16 inputs/outputs and <= 1e-4 for the fp32 path.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention_jvp
+from paper_2606_25473_amd import attn_fwd, attn_jvp_fwd
+from paper_2606_25473_amd.workloads import (MASK_BLOCK_CAUSAL, MASK_FULL, MASK_TEACHER_FORCING, WORKLOADS,
+                                            custom_workload, make_inputs)
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"bf16": 1e-2, "f32": 1e-4}
+
+
+def _say(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def _rel(x, ref):
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    return float(np.linalg.norm(x - ref) / max(np.linalg.norm(ref), 1e-300))
+
+
+def _np(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def _offsets(w):
+    return list(w.offsets) if w.offsets else None
+
+
+def _run_gpu(w, x):
+    g = {k: v.cuda() for k, v in x.items()}
+    o, do, lse = attn_jvp_fwd(g["Q"], g["K"], g["V"], g["dQ"], g["dK"], g["dV"], w.kind, _offsets(w))
+    torch.cuda.synchronize()
+    return o, do, lse
+
+
+def _check_full(w, seed=0):
+    _say(f"[parity] {w.name} B={w.B} H={w.H} L={w.L} D={w.D} {w.dtype} {w.kind} offsets={w.offsets[:6]}")
+    x = make_inputs(w, "cpu", seed)
+    o, do, lse = _run_gpu(w, x)
+    O, dO, LSE = attention_jvp(*[_np(x[k]) for k in ("Q", "K", "V", "dQ", "dK", "dV")], w.kind, _offsets(w))
+    errs = (_rel(_np(o), O), _rel(_np(do), dO), _rel(_np(lse), LSE))
+    _say(f"[parity] {w.name} rel-L2 O={errs[0]:.3e} dO={errs[1]:.3e} LSE={errs[2]:.3e}")
+    tol = TOL[w.dtype]
+    assert max(errs) <= tol, errs
+    return x, (o, do, lse)
+
+
+EDGE = [
+    custom_workload("tf_ragged_bf16", 2, 2, 128, "bf16", MASK_TEACHER_FORCING, 3, 100, tangent_std=0.5),
+    custom_workload("tf_several_tiles_bf16", 1, 3, 128, "bf16", MASK_TEACHER_FORCING, 4, 300, tangent_std=0.5),
+    custom_workload("tf_one_token_chunks_bf16", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, 64, 1, tangent_std=0.5),
+    custom_workload("tf_one_chunk_bf16", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, 1, 300, tangent_std=0.5),
+    custom_workload("tf_nonuniform_bf16", 1, 2, 128, "bf16", MASK_TEACHER_FORCING,
+                    offsets=[0, 1, 3, 7, 40, 41, 90, 200], tangent_std=0.5),
+    custom_workload("tf_d64_bf16", 1, 2, 64, "bf16", MASK_TEACHER_FORCING, 4, 50, tangent_std=0.5),
+    custom_workload("block_causal_bf16", 1, 2, 128, "bf16", MASK_BLOCK_CAUSAL,
+                    offsets=[0, 50, 77, 200, 333], tangent_std=0.5),
+    custom_workload("full_1000_bf16", 1, 2, 128, "bf16", MASK_FULL, L=1000, tangent_std=0.5),
+    custom_workload("full_below_one_tile_bf16", 1, 1, 128, "bf16", MASK_FULL, L=7, tangent_std=0.5),
+    custom_workload("full_single_token_bf16", 1, 1, 128, "bf16", MASK_FULL, L=1, tangent_std=0.5),
+    custom_workload("full_d64_bf16", 2, 1, 64, "bf16", MASK_FULL, L=333, tangent_std=0.5),
+    custom_workload("tf_f32_d128", 1, 2, 128, "f32", MASK_TEACHER_FORCING, 3, 20),
+    custom_workload("full_f32_d64", 1, 2, 64, "f32", MASK_FULL, L=50),
+    custom_workload("block_causal_f32", 1, 1, 64, "f32", MASK_BLOCK_CAUSAL, offsets=[0, 3, 10, 31]),
+]
+
+
+def test_tiny_tf_fp32_workload():
+    """The 4-chunk x 16-token fp32 TF workload, seed 0, against the oracle to 1e-4."""
+    _check_full(WORKLOADS["tiny_tf"])
+
+
+@pytest.mark.parametrize("w", EDGE, ids=[w.name for w in EDGE])
+def test_edge_shapes(w):
+    _check_full(w, seed=1)
+
+
+def test_zero_tangents_give_exact_zero():
+    for dt in ("bf16", "f32"):
+        w = custom_workload(f"zero_tangent_{dt}", 1, 2, 128, dt, MASK_TEACHER_FORCING, 3, 100)
+        _say(f"[invariant] zero tangents {dt}")
+        x = make_inputs(w, "cpu", 3)
+        for k in ("dQ", "dK", "dV"):
+            x[k] = torch.zeros_like(x[k])
+        _, do, _ = _run_gpu(w, x)
+        assert torch.count_nonzero(do).item() == 0
+
+
+def test_forward_matches_jvp_primal_and_oracle():
+    w = custom_workload("fwd_vs_jvp", 2, 2, 128, "bf16", MASK_TEACHER_FORCING, 3, 100, tangent_std=0.5)
+    _say("[invariant] attn_fwd vs attn_jvp_fwd primal")
+    x = make_inputs(w, "cpu", 4)
+    o, _, lse = _run_gpu(w, x)
+    g = {k: v.cuda() for k, v in x.items()}
+    of, lsef = attn_fwd(g["Q"], g["K"], g["V"], w.kind, _offsets(w))
+    torch.cuda.synchronize()
+    # same operations in the same order for the primal part
+    assert _rel(_np(of), _np(o)) < 1e-3
+    assert _rel(_np(lsef), _np(lse)) < 1e-6
+    O, _, LSE = attention_jvp(*[_np(x[k]) for k in ("Q", "K", "V", "dQ", "dK", "dV")], w.kind, _offsets(w))
+    assert _rel(_np(of), O) < TOL["bf16"] and _rel(_np(lsef), LSE) < TOL["bf16"]
+
+
+def test_deterministic_run_to_run():
+    w = custom_workload("determinism", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, 4, 150, tangent_std=0.5)
+    _say("[invariant] determinism")
+    x = make_inputs(w, "cpu", 5)
+    a = _run_gpu(w, x)
+    b = _run_gpu(w, x)
+    for u, v in zip(a, b):
+        assert torch.equal(u, v)
+
+
+def test_clean_half_independent_of_noisy_inputs():
+    w = custom_workload("clean_half", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, 3, 100, tangent_std=0.5)
+    _say("[invariant] clean half independent of noisy inputs")
+    x = make_inputs(w, "cpu", 6)
+    a = _run_gpu(w, x)
+    half = w.L // 2
+    y = {k: v.clone() for k, v in x.items()}
+    gen = torch.Generator().manual_seed(99)
+    for k in y:
+        y[k][:, :, half:] = torch.randn(y[k][:, :, half:].shape, generator=gen).to(y[k].dtype)
+    b = _run_gpu(w, y)
+    for u, v in zip(a, b):
+        assert torch.equal(u[:, :, :half], v[:, :, :half])
+
+
+def test_tangent_linearity():
+    w = custom_workload("linearity", 1, 2, 128, "f32", MASK_TEACHER_FORCING, 3, 40)
+    _say("[invariant] linearity (fp32 path)")
+    x = make_inputs(w, "cpu", 7)
+    _, d1, _ = _run_gpu(w, x)
+    y = dict(x)
+    for k in ("dQ", "dK", "dV"):
+        y[k] = 2.5 * x[k]
+    _, d2, _ = _run_gpu(w, y)
+    assert _rel(_np(d2), 2.5 * _np(d1)) < 1e-5
+
+
+# ----------------------------------------------------------------------------- full-size workloads
+
+def _sample_rows(w, n_random=24, seed=0):
+    L = w.L
+    rows = {0, L - 1}
+    if w.kind == MASK_TEACHER_FORCING:
+        half = w.offsets[-1]
+        for o in w.offsets:
+            for base in (0, half):
+                for d in (-1, 0, 1):
+                    r = base + o + d
+                    if 0 <= r < L:
+                        rows.add(r)
+    for t in range(0, L, 128 * 97):
+        rows.add(t)
+    rng = np.random.default_rng(seed)
+    rows.update(int(r) for r in rng.integers(0, L, n_random))
+    return np.array(sorted(rows))
+
+
+FULL_SIZE = ["wan1.3b_chunkwise_tf", "wan1.3b_framewise_tf", "wan1.3b_bidirectional", "wan14b_chunkwise_tf"]
+
+
+@pytest.mark.parametrize("name", FULL_SIZE)
+def test_full_size_sampled_rows(name):
+    w = WORKLOADS[name]
+    _say(f"[full-size] {name} B={w.B} H={w.H} L={w.L}: generating inputs on the GPU")
+    x = make_inputs(w, "cuda", 0)
+    o, do, lse = attn_jvp_fwd(x["Q"], x["K"], x["V"], x["dQ"], x["dK"], x["dV"], w.kind, _offsets(w))
+    torch.cuda.synchronize()
+    _say(f"[full-size] {name}: kernel done, checking finiteness and sampled rows")
+    assert torch.isfinite(o).all() and torch.isfinite(do).all() and torch.isfinite(lse).all()
+    rows = _sample_rows(w)
+    heads = sorted({(0, 0), (w.B - 1, w.H - 1), (w.B // 2, w.H // 2)})
+    fwd = attn_fwd(x["Q"], x["K"], x["V"], w.kind, _offsets(w)) if name == "wan14b_chunkwise_tf" else None
+    torch.cuda.synchronize()
+    ridx = torch.from_numpy(rows).cuda()
+    for b, h in heads:
+        sl = {k: _np(v[b:b + 1, h:h + 1]) for k, v in x.items()}
+        O, dO, LSE = attention_jvp(sl["Q"], sl["K"], sl["V"], sl["dQ"], sl["dK"], sl["dV"], w.kind,
+                                   _offsets(w), rows=rows)
+        got = (_np(o[b, h].index_select(0, ridx)), _np(do[b, h].index_select(0, ridx)),
+               _np(lse[b, h].index_select(0, ridx)))
+        errs = (_rel(got[0], O[0, 0]), _rel(got[1], dO[0, 0]), _rel(got[2], LSE[0, 0]))
+        _say(f"[full-size] {name} (b={b}, h={h}) {len(rows)} rows rel-L2 O={errs[0]:.3e} "
+             f"dO={errs[1]:.3e} LSE={errs[2]:.3e}")
+        assert max(errs) <= TOL["bf16"], errs
+        if fwd is not None:
+            ef = (_rel(_np(fwd[0][b, h].index_select(0, ridx)), O[0, 0]),
+                  _rel(_np(fwd[1][b, h].index_select(0, ridx)), LSE[0, 0]))
+            _say(f"[full-size] {name} attn_fwd (b={b}, h={h}) rel-L2 O={ef[0]:.3e} LSE={ef[1]:.3e}")
+            assert max(ef) <= TOL["bf16"], ef

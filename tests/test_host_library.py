@@ -1,0 +1,183 @@
+"""CPU tests of the C-ABI library: symbols, host-side layout logic and error paths.
+
+No kernel runs here.  Every call either is host-only (pair counts, group table,
+tile plans) or fails argument validation, which happens before any HIP call.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import MASK_BLOCK_CAUSAL, MASK_FULL, MASK_TEACHER_FORCING, allowed_mask, count_allowed_pairs
+from paper_2606_25473_amd import binding
+from paper_2606_25473_amd.binding import make_layout
+from paper_2606_25473_amd.workloads import WORKLOADS
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "attn_jvp.h")
+
+LAYOUTS = [
+    (MASK_TEACHER_FORCING, [0, 16, 32, 48, 64], 128),
+    (MASK_TEACHER_FORCING, [0, 100, 200, 300], 600),
+    (MASK_TEACHER_FORCING, [0, 1, 3, 7, 40, 41, 90, 200], 400),
+    (MASK_TEACHER_FORCING, list(range(65)), 128),          # C = 1, N = 64
+    (MASK_TEACHER_FORCING, [0, 300], 600),                  # N = 1
+    (MASK_BLOCK_CAUSAL, [0, 50, 77, 200, 333], 333),
+    (MASK_FULL, None, 1000),
+    (MASK_FULL, None, 7),
+]
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return binding.load_library()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return re.findall(r"^\s*(?:const\s+)?[a-z0-9_]+\s*\*?\s*(attn_[a-z_]+)\s*\(", text, flags=re.M)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    names = _declared_functions()
+    assert {"attn_jvp_fwd", "attn_fwd", "attn_count_unmasked_pairs", "attn_last_error"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in attn_jvp.h but not exported"
+
+
+@pytest.mark.parametrize("kind,offsets,L", LAYOUTS)
+def test_unmasked_pair_count_matches_brute_force(lib, kind, offsets, L):
+    assert binding.count_unmasked_pairs(kind, offsets, L) == count_allowed_pairs(kind, offsets, L)
+
+
+@pytest.mark.parametrize("name", ["tiny_tf", "wan1.3b_chunkwise_tf", "wan1.3b_framewise_tf",
+                                  "wan1.3b_bidirectional", "wan14b_chunkwise_tf"])
+def test_workload_pair_counts_closed_form(lib, name):
+    w = WORKLOADS[name]
+    n = binding.count_unmasked_pairs(w.kind, list(w.offsets) or None, w.L)
+    if w.kind == MASK_FULL:
+        assert n == w.L * w.L
+    else:
+        C, N = w.offsets[1], w.num_chunks
+        assert n == C * C * N * (N + 1)
+
+
+@pytest.mark.parametrize("kind,offsets,L", LAYOUTS)
+def test_query_groups_reproduce_mask(lib, kind, offsets, L):
+    groups = binding.query_groups(kind, offsets, L)
+    m = np.zeros((L, L), dtype=bool)
+    prev = 0
+    for q0, q1, a0, a1, b0, b1 in groups:
+        assert q0 == prev and q1 > q0
+        prev = q1
+        m[q0:q1, a0:a1] = True
+        m[q0:q1, b0:b1] = True
+    assert prev == L
+    assert np.array_equal(m, allowed_mask(kind, offsets, L))
+
+
+@pytest.mark.parametrize("kind,offsets,L", LAYOUTS)
+def test_tile_plans_cover_mask_and_full_blocks_are_full(lib, kind, offsets, L):
+    R, C = binding.tile_shape()
+    mask = allowed_mask(kind, offsets, L)
+    computed = 0
+    for t in range((L + R - 1) // R):
+        rows = slice(t * R, min(L, t * R + R))
+        plan = binding.tile_plan(kind, offsets, L, t)
+        blocks = [b for b, _ in plan]
+        assert blocks == sorted(set(blocks)), "blocks visited once, in key order"
+        visited = np.zeros(L, dtype=bool)
+        for b, full in plan:
+            visited[b * C:(b + 1) * C] = True
+            if full:
+                assert b * C + C <= L and mask[rows, b * C:b * C + C].all()
+            computed += (rows.stop - rows.start) * min(C, L - b * C)
+        # every admissible pair of the tile lies in a visited block
+        assert not (mask[rows] & ~visited[None, :]).any()
+    assert computed == binding.count_computed_pairs(kind, offsets, L)
+
+
+def test_computed_pair_overhead_on_wan_chunkwise(lib):
+    w = WORKLOADS["wan1.3b_chunkwise_tf"]
+    un = binding.count_unmasked_pairs(w.kind, w.offsets, w.L)
+    comp = binding.count_computed_pairs(w.kind, w.offsets, w.L)
+    assert 1.0 <= comp / un < 1.02
+
+
+# ----------------------------------------------------------------------------- error paths
+
+FAKE = 1 << 40          # never dereferenced: every call below fails validation first
+
+# Belt and braces: these calls pass fake device pointers, so never run them where a
+# GPU could actually receive a launch if a case were wrongly accepted.
+_no_gpu = pytest.mark.skipif(__import__("torch").cuda.is_available(),
+                             reason="fake-pointer validation tests run on CPU-only hosts")
+
+
+def _ptrs(n=9, dtype_bytes=2, B=1, H=1, L=64, D=64):
+    span = B * H * L * D * dtype_bytes
+    return [FAKE + i * (span + 4096) for i in range(n)]
+
+
+def _with(i, value):
+    """The 9 pointers Q, K, V, dQ, dK, dV, O, dO, LSE with entry i replaced."""
+    p = _ptrs()
+    p[i] = value
+    return p
+
+
+def _call(lib, **kw):
+    dtype, B, H, L, D = kw.get("dtype", 1), kw.get("B", 1), kw.get("H", 1), kw.get("L", 64), kw.get("D", 64)
+    es = 4 if dtype == 0 else 2
+    p = kw.get("ptrs") or _ptrs(9, es, B, H, L, D)
+    layout = kw.get("layout") or make_layout("full")
+    return lib.attn_jvp_fwd(dtype, B, H, L, D, p[0], p[1], p[2], p[3], p[4], p[5],
+                            ctypes.byref(layout), 0.0, p[6], p[7], p[8], None)
+
+
+@pytest.mark.parametrize("kw,code,needle", [
+    (dict(dtype=7), 2, "dtype"),
+    (dict(D=96), 2, "head_dim"),
+    (dict(L=0), 1, "positive"),
+    (dict(B=-1), 1, "positive"),
+    (dict(ptrs=_with(0, 0)), 1, "NULL"),
+    (dict(ptrs=_with(5, 0)), 1, "NULL"),
+    (dict(ptrs=_with(0, FAKE + 2)), 1, "aligned"),
+    (dict(ptrs=_with(6, _ptrs()[0])), 1, "overlaps input"),
+    (dict(ptrs=_with(7, _ptrs()[6] + 64)), 1, "overlap"),
+    (dict(layout=make_layout("teacher_forcing", [0, 16, 40])), 1, "L = 2"),
+    (dict(layout=make_layout("teacher_forcing", [0, 16, 16, 32]), L=64), 1, "increasing"),
+    (dict(layout=make_layout("teacher_forcing", [5, 16, 32]), L=64), 1, "must be 0"),
+    (dict(layout=make_layout("block_causal", [0, 10, 20]), L=64), 1, "block-causal"),
+    (dict(layout=make_layout("teacher_forcing", list(range(66))), L=130), 1, "num_chunks"),
+    (dict(layout=make_layout(9)), 1, "kind"),
+])
+@_no_gpu
+def test_invalid_arguments_are_rejected_before_any_hip_call(lib, kw, code, needle):
+    rc = _call(lib, **kw)
+    assert rc == code
+    assert needle in binding.last_error()
+
+
+@_no_gpu
+def test_forward_entry_point_validates_too(lib):
+    p = _ptrs(5)
+    rc = lib.attn_fwd(1, 1, 1, 64, 80, p[0], p[1], p[2], ctypes.byref(make_layout("full")), 0.0, p[3], p[4], None)
+    assert rc == 2 and "head_dim" in binding.last_error()
+
+
+def test_host_queries_reject_bad_layouts(lib):
+    with pytest.raises(binding.AttnError):
+        binding.count_unmasked_pairs("teacher_forcing", [0, 10, 5], 20)
+    with pytest.raises(binding.AttnError):
+        binding.tile_plan("full", None, 100, 1)
+    assert lib.attn_count_computed_pairs(ctypes.byref(make_layout("full")), 100, 32) == -1
+
+
+def test_python_binding_refuses_cpu_tensors():
+    import torch
+    x = torch.zeros(1, 1, 8, 64)
+    with pytest.raises(ValueError):
+        binding.attn_jvp_fwd(x, x, x, x, x, x, "full")
