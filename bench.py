@@ -1,0 +1,191 @@
+"""Throughput of the fused masked attention forward + JVP on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--forward] [--no-cpu]
+
+One step = one ``attn_jvp_fwd`` call over the whole batch of the workload
+(default: Wan2.1-1.3B chunk-wise teacher forcing, B=1, H=12, L=65520, D=128,
+bf16), inputs already resident in HBM.  Work is counted over admissible
+(query, key) pairs only: 12*D flop per pair for the JVP, 4*D for the forward.
+Prints ONE JSON line.  The ``cpu_baseline`` leg times the fp64 CPU oracle on a
+bounded sample of query rows of the same workload (and checks the sampled GPU
+rows against it).
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2606_25473_amd import attn_fwd, attn_jvp_fwd, count_computed_pairs, count_unmasked_pairs  # noqa: E402
+from paper_2606_25473_amd.workloads import HEADLINE, WORKLOADS, make_inputs  # noqa: E402
+
+METRIC = "masked attention fwd+JVP TFLOP/s (unmasked pairs) and % bf16 MFMA peak"
+# MI355X dense bf16 matrix peak: 256 CUs x 2.4 GHz x 4096 flop/clk/CU
+PEAK_BF16_TFLOPS = 256 * 2.4e9 * 4096 / 1e12
+PEAK_FP32_TFLOPS = 157.3
+KERNEL_SOURCES = ["paper_2606_25473_amd/csrc/attn_mfma.hip", "paper_2606_25473_amd/csrc/schedule.hpp",
+                  "paper_2606_25473_amd/csrc/kernels.hpp"]
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, forward):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    key = f"{workload}:{'fwd' if forward else 'jvp'}"
+    ent = rec.get(key)
+    if not ent or ent.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return ent.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, x, out, forward, budget_s=15.0):
+    """Time the fp64 CPU oracle on a bounded sample of rows of head (0, 0)."""
+    from oracle import allowed_mask, attention_fwd, attention_jvp  # the oracle is only used on this leg
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        cores = int(blas[0]["num_threads"]) if blas else os.cpu_count()
+        blas_name = blas[0].get("internal_api", "?") if blas else "?"
+    except Exception:  # threadpoolctl missing
+        cores, blas_name = os.cpu_count(), "?"
+    L = w.L
+    h = {k: v[0:1, 0:1].float().cpu().numpy() for k, v in x.items()}
+    offs = list(w.offsets) or None
+    # rows spread evenly over the sequence so the per-row key-count mix matches the workload
+    order = np.random.default_rng(0).permutation(L)
+    done, t_used, pairs, flop_per_pair = 0, 0.0, 0, (4 if forward else 12) * w.D
+    errs = []
+    got_o, got_do = out[0][0, 0], (None if forward else out[1][0, 0])
+    batch = 256
+    while t_used < budget_s and done < L:
+        rows = np.sort(order[done:done + batch])
+        t0 = time.perf_counter()
+        if forward:
+            O, _ = attention_fwd(h["Q"], h["K"], h["V"], w.kind, offs, rows=rows)
+            dO = None
+        else:
+            O, dO, _ = attention_jvp(h["Q"], h["K"], h["V"], h["dQ"], h["dK"], h["dV"], w.kind, offs, rows=rows)
+        t_used += time.perf_counter() - t0
+        done += len(rows)
+        pairs += int(allowed_mask(w.kind, offs, L, rows).sum())
+        r = torch.from_numpy(rows).to(got_o.device)
+        g = got_o.index_select(0, r).float().cpu().numpy()
+        errs.append((np.linalg.norm(g - O[0, 0]) ** 2, np.linalg.norm(O[0, 0]) ** 2))
+        if dO is not None:
+            gd = got_do.index_select(0, r).float().cpu().numpy()
+            errs.append((np.linalg.norm(gd - dO[0, 0]) ** 2, np.linalg.norm(dO[0, 0]) ** 2))
+    rel = float(np.sqrt(sum(e for e, _ in errs) / max(sum(n for _, n in errs), 1e-300)))
+    value = pairs * flop_per_pair / t_used / 1e12
+    return {"value": value, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": f"{done} query rows of head (0,0) spread over the {L}-token sequence "
+                      f"({pairs} admissible pairs, {t_used:.1f} s, fp64 numpy/{blas_name})",
+            "sample_rel_l2_vs_gpu": rel}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=HEADLINE, choices=sorted(WORKLOADS))
+    ap.add_argument("--forward", action="store_true", help="time attn_fwd instead of attn_jvp_fwd")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the kernel runs on one "
+              "GPU's share of heads and multi-GPU runs are not part of this build.", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+
+    w = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    x = make_inputs(w, "cuda", seed=0)
+    offs = list(w.offsets) or None
+    q, k, v, dq, dk, dv = (x[n] for n in ("Q", "K", "V", "dQ", "dK", "dV"))
+    B, H, L, D = q.shape
+    o = torch.empty_like(q)
+    do = torch.empty_like(q)
+    lse = torch.empty((B, H, L), device=dev, dtype=torch.float32)
+
+    def step():
+        if args.forward:
+            attn_fwd(q, k, v, w.kind, offs, out=(o, lse))
+        else:
+            attn_jvp_fwd(q, k, v, dq, dk, dv, w.kind, offs, out=(o, do, lse))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for i in range(args.steps):
+        step()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    kernel_ms = ev[0].elapsed_time(ev[-1]) / args.steps
+    ms_per_step = wall * 1e3 / args.steps
+
+    pairs = count_unmasked_pairs(w.kind, offs, L)
+    computed = count_computed_pairs(w.kind, offs, L, D)
+    flop_per_pair = (4 if args.forward else 12) * D
+    flop = pairs * flop_per_pair * B * H
+    value = flop / (ms_per_step * 1e-3) / 1e12
+    achieved = flop / (kernel_ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_TFLOPS
+    traffic = measured_traffic(w.name, args.forward)
+    res = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": dict(w.describe(), op="attn_fwd" if args.forward else "attn_jvp_fwd"),
+        "pct_peak": round(100 * achieved / peak, 2),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": round(peak, 1),
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": traffic},
+        "kernel_ms": {"mean": round(kernel_ms, 4), "median": round(float(np.median(per)), 4),
+                      "min": round(min(per), 4)},
+        "unmasked_pairs_per_head": pairs,
+        "computed_over_unmasked": round(computed / pairs, 4),
+    }
+    if not args.no_cpu:
+        res["cpu_baseline"] = cpu_baseline(w, x, (o, do, lse), args.forward, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()
