@@ -102,9 +102,13 @@ template <int D, bool JVP>
 __global__ __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attn_mfma_kernel(const AttnArgs a) {
   using G = Geo<D>;
-  constexpr int NTILE = JVP ? 4 : 2;  // K, V (, dK, dV) per stage
-  constexpr int STAGEB = NTILE * G::TILEB;
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGEB];
+  constexpr int TB = G::TILEB;
+  constexpr int TBJ = JVP ? G::TILEB : 16;  // tangent tiles exist only in the JVP kernel
+  // Two pipeline stages, each tile its own LDS object: the compiler then knows that
+  // the loads streaming into one stage never alias the reads of the other, and does
+  // not wait for the prefetch before reading the current stage.
+  __shared__ __attribute__((aligned(1024))) char sK0[TB], sV0[TB], sK1[TB], sV1[TB];
+  __shared__ __attribute__((aligned(1024))) char sdK0[TBJ], sdV0[TBJ], sdK1[TBJ], sdV1[TBJ];
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -141,41 +145,45 @@ void attn_mfma_kernel(const AttnArgs a) {
   bf16x8 qop[G::KS], dqop[JVP ? G::KS : 1];
 #pragma unroll
   for (int s = 0; s < G::KS; ++s) {
-    if (row < L) {
-      qop[s] = *(const bf16x8*)(Qg + (size_t)row * D + 16 * s + 8 * hh);
-      if constexpr (JVP) dqop[s] = *(const bf16x8*)(dQg + (size_t)row * D + 16 * s + 8 * hh);
-    } else {
-      qop[s] = bf16x8{};
-      if constexpr (JVP) dqop[s] = bf16x8{};
-    }
+    // rows past the end are clamped to the last row (their outputs are not stored)
+    const size_t qoff = (size_t)min(row, L - 1) * D + 16 * s + 8 * hh;
+    qop[s] = *(const bf16x8*)(Qg + qoff);
+    if constexpr (JVP) dqop[s] = *(const bf16x8*)(dQg + qoff);
   }
 
-  // ---- global -> register -> LDS staging of one key block
-  u32x4 stg[NTILE][G::CPTH];
-  auto load_block = [&](int kb) {
-    const int k0 = kb * BC;
+  // ---- global -> LDS staging of one key block: direct loads (global_load_lds_dwordx4).
+  // One wave instruction writes 64 lanes x 16 bytes = 1 KiB of consecutive LDS, i.e.
+  // 1024 / ROWB rows; the XOR swizzle is realised by choosing which logical chunk
+  // each lane fetches.  Keys past the end of the sequence are clamped to the last
+  // key (finite data; those keys are masked out of the softmax).
+  constexpr int IPT = G::TILEB / 1024;        // wave instructions per tile
+  constexpr int IPW = IPT / 4;                // per wave (4 waves)
+  static_assert(IPT % 4 == 0, "tile must split evenly over the 4 waves");
+  int dma_row[IPW], dma_col[IPW];
 #pragma unroll
-    for (int t = 0; t < NTILE; ++t) {
-      const bf16_t* src = t == 0 ? Kg : t == 1 ? Vg : t == 2 ? dKg : dVg;
+  for (int j = 0; j < IPW; ++j) {
+    const int byte = (wave * IPW + j) * 1024 + lane * 16;
+    const int r = byte / G::ROWB;
+    const int phys = (byte % G::ROWB) >> 4;
+    dma_row[j] = r;
+    dma_col[j] = (phys ^ swz<D>(r)) * 8;
+  }
+  auto dma_tile = [&](const bf16_t* src, int k0, char* dst) {
 #pragma unroll
-      for (int j = 0; j < G::CPTH; ++j) {
-        const int cid = tid + NTHREADS * j;
-        const int r = cid / G::NCH, c = cid % G::NCH;
-        const int key = k0 + r;
-        stg[t][j] = key < L ? *(const u32x4*)(src + (size_t)key * D + c * 8) : u32x4{0u, 0u, 0u, 0u};
-      }
+    for (int j = 0; j < IPW; ++j) {
+      const int key = min(k0 + dma_row[j], L - 1);
+      __builtin_amdgcn_global_load_lds(
+          (const __attribute__((address_space(1))) void*)(src + (size_t)key * D + dma_col[j]),
+          (__attribute__((address_space(3))) void*)(dst + (wave * IPW + j) * 1024), 16, 0, 0);
     }
   };
-  auto store_block = [&](int st) {
-    char* base = smem + st * STAGEB;
-#pragma unroll
-    for (int t = 0; t < NTILE; ++t) {
-#pragma unroll
-      for (int j = 0; j < G::CPTH; ++j) {
-        const int cid = tid + NTHREADS * j;
-        const int r = cid / G::NCH, c = cid % G::NCH;
-        *(u32x4*)(base + t * G::TILEB + lds_off<D>(r, c)) = stg[t][j];
-      }
+  auto dma_block = [&](int kb, char* k, char* v, char* dk, char* dv) {
+    const int k0 = kb * BC;
+    dma_tile(Kg, k0, k);
+    dma_tile(Vg, k0, v);
+    if constexpr (JVP) {
+      dma_tile(dKg, k0, dk);
+      dma_tile(dVg, k0, dv);
     }
   };
 
@@ -204,88 +212,73 @@ void attn_mfma_kernel(const AttnArgs a) {
   float m = -INFINITY;  // running reference max (log2 units); equal in lanes l and l^32
   float lsum = 0.f;     // partial normaliser over this lane's keys
   float rsum = 0.f;     // partial sum of P~ o dS over this lane's keys
+  float mpend = 0.f;    // block max that triggered a rescale
   const float c2 = a.scale * kLog2e;
   const float sc = a.scale;
+  const int krow = lane & 31;
 
-  if (nblk > 0) {
-    load_block(plan_block(plan, 0));
-    store_block(0);
-  }
-  __syncthreads();
-
-  for (int it = 0; it < nblk; ++it) {
-    const int st = it & 1;
-    const bool more = it + 1 < nblk;
-    if (more) load_block(plan_block(plan, it + 1));
-
-    const int kb = plan_block(plan, it);
-    const int k0 = kb * BC;
-    const char* sK = smem + st * STAGEB;
-    const char* sV = sK + G::TILEB;
-    const char* sdK = sK + 2 * G::TILEB;
-    const char* sdV = sK + 3 * G::TILEB;
+  // One key block.  Returns true -- before touching any accumulator -- if some row's
+  // block max exceeds its reference by more than kLazy; the caller then rescales and
+  // redoes the block.
+  auto step = [&](int it, const char* cK, const char* cV, const char* cdK, const char* cdV,
+                  char* nK, char* nV, char* ndK, char* ndV) -> bool {
+    // prefetch the next block into the other stage (free since the last barrier)
+    if (it + 1 < nblk) dma_block(plan_block(plan, it + 1), nK, nV, ndK, ndV);
+    const int k0 = plan_block(plan, it) * BC;
 
     // ---- scores and score tangents (transposed): S^T = K Q^T, dS^T = dK Q^T + K dQ^T
     f32x16 S = f32x16{}, dS = f32x16{};
-    const int krow = lane & 31;
 #pragma unroll
     for (int s = 0; s < G::KS; ++s) {
       const int off = lds_off<D>(krow, 2 * s + hh);
-      const bf16x8 kop = *(const bf16x8*)(sK + off);
+      const bf16x8 kop = *(const bf16x8*)(cK + off);
       S = mfma(kop, qop[s], S);
       if constexpr (JVP) {
-        const bf16x8 dkop = *(const bf16x8*)(sdK + off);
+        const bf16x8 dkop = *(const bf16x8*)(cdK + off);
         dS = mfma(dkop, qop[s], dS);
         dS = mfma(kop, dqop[s], dS);
       }
     }
 
-    // ---- mask (only on blocks not admissible for every row of the tile)
-    float s2[16];
+    // ---- mask (only on blocks not admissible for every row of the tile): S = -inf, dS = 0
+    float sv[16], dsv[16];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) s2[i] = S[i] * c2;
+    for (int i = 0; i < 16; ++i) {
+      sv[i] = S[i];
+      dsv[i] = JVP ? dS[i] : 0.f;
+    }
     if (!block_is_full(plan, k0, BC, L)) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int key = k0 + 8 * (i >> 2) + 4 * hh + (i & 3);
-        const bool ok = key < L && ((key >= ra0 && key < ra1) || (key >= rb0 && key < rb1));
-        if (!ok) {
-          s2[i] = -INFINITY;
-          if constexpr (JVP) dS[i] = 0.f;
-        }
+        const bool ok = (unsigned)(key - ra0) < (unsigned)(ra1 - ra0) ||
+                        (unsigned)(key - rb0) < (unsigned)(rb1 - rb0);
+        sv[i] = ok ? sv[i] : -INFINITY;
+        dsv[i] = ok ? dsv[i] : 0.f;
       }
     }
 
-    // ---- online softmax with lazy rescaling
-    float mx = s2[0];
+    // ---- online softmax.  The scale is positive, so max(S) * c2 = max(S * c2).
+    float mxr = sv[0];
 #pragma unroll
-    for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s2[i]);
-    mx = fmaxf(mx, xor32(mx));
-    const bool up = mx > m + kLazy;
-    if (__ballot(up)) {
-      const float mnew = up ? mx : m;
-      const float alpha = up ? __builtin_amdgcn_exp2f(m - mnew) : 1.f;
-      lsum *= alpha;
-      if constexpr (JVP) rsum *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < G::DT; ++dt) {
-        oacc[dt] *= alpha;
-        if constexpr (JVP) tacc[dt] *= alpha;
-      }
-      m = mnew;
+    for (int i = 1; i < 16; ++i) mxr = fmaxf(mxr, sv[i]);
+    const float mloc = mxr * c2;
+    if (__ballot(mloc > m + kLazy) != 0) {
+      mpend = mloc;
+      return true;
     }
-    const float mref = m == -INFINITY ? 0.f : m;
+    const float mneg = m == -INFINITY ? 0.f : -m;
     float p[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      p[i] = __builtin_amdgcn_exp2f(s2[i] - mref);
+      p[i] = __builtin_amdgcn_exp2f(fmaf(sv[i], c2, mneg));
       lsum += p[i];
     }
     float hv[16];
     if constexpr (JVP) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        hv[i] = p[i] * (dS[i] * sc);
+        hv[i] = p[i] * (dsv[i] * sc);
         rsum += hv[i];
       }
     }
@@ -301,18 +294,56 @@ void attn_mfma_kernel(const AttnArgs a) {
       }
 #pragma unroll
       for (int dt = 0; dt < G::DT; ++dt) {
-        const bf16x8 vop = cat(ld_tr(sV + tro[t][0][dt]), ld_tr(sV + tro[t][1][dt]));
+        const bf16x8 vop = cat(ld_tr(cV + tro[t][0][dt]), ld_tr(cV + tro[t][1][dt]));
         oacc[dt] = mfma(vop, pb, oacc[dt]);
         if constexpr (JVP) {
-          const bf16x8 dvop = cat(ld_tr(sdV + tro[t][0][dt]), ld_tr(sdV + tro[t][1][dt]));
+          const bf16x8 dvop = cat(ld_tr(cdV + tro[t][0][dt]), ld_tr(cdV + tro[t][1][dt]));
           tacc[dt] = mfma(dvop, pb, tacc[dt]);
           tacc[dt] = mfma(vop, hb, tacc[dt]);
         }
       }
     }
 
-    if (more) store_block(st ^ 1);
-    __syncthreads();
+    __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): the prefetch into the other stage has landed
+    __syncthreads();                    // ... for every wave, and nobody reads this stage any more
+    return false;
+  };
+
+  if (nblk > 0) dma_block(plan_block(plan, 0), sK0, sV0, sdK0, sdV0);
+  __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): this wave's LDS loads have landed
+  __syncthreads();
+
+  int it = 0;
+  while (it < nblk) {
+    // hot loop, unrolled by two so that every LDS access names its stage statically
+    bool rescale = false;
+    if (it & 1) {
+      rescale = step(it, sK1, sV1, sdK1, sdV1, sK0, sV0, sdK0, sdV0);
+      if (!rescale) ++it;
+    }
+    while (!rescale && it < nblk) {
+      rescale = step(it, sK0, sV0, sdK0, sdV0, sK1, sV1, sdK1, sdV1);
+      if (rescale || ++it >= nblk) break;
+      rescale = step(it, sK1, sV1, sdK1, sdV1, sK0, sV0, sdK0, sdV0);
+      if (!rescale) ++it;
+    }
+    if (!rescale) break;
+    // Cold path: move the reference max of the rows that need it (lanes l and l^32 hold
+    // the same query, so the new reference is their joint max), rescale O, T, l, r, and
+    // redo block `it` (its S is recomputed; the stage still holds its K/V, and the
+    // repeated prefetch rewrites the other stage with identical data).
+    const float mx = fmaxf(mpend, xor32(mpend));
+    const bool up = mx > m + kLazy;
+    const float mnew = up ? mx : m;
+    const float alpha = up ? __builtin_amdgcn_exp2f(m - mnew) : 1.f;
+    lsum *= alpha;
+    if constexpr (JVP) rsum *= alpha;
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt) {
+      oacc[dt] *= alpha;
+      if constexpr (JVP) tacc[dt] *= alpha;
+    }
+    m = mnew;
   }
 
   // ---- epilogue: combine the two half-waves' partial sums, normalise, store
