@@ -110,6 +110,8 @@ def main():
     ap.add_argument("--forward", action="store_true", help="time attn_fwd instead of attn_jvp_fwd")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="first run one plain device copy of this many MiB (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the kernel runs on one "
@@ -135,6 +137,15 @@ def main():
             attn_fwd(q, k, v, w.kind, offs, out=(o, lse))
         else:
             attn_jvp_fwd(q, k, v, dq, dk, dv, w.kind, offs, out=(o, do, lse))
+
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib * (1 << 20)
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)  # reads n bytes, writes n bytes
+        torch.cuda.synchronize()
+        del src, dst
 
     for _ in range(args.warmup):
         step()

@@ -1,0 +1,113 @@
+"""Summarise rocprofv3 CSV output of a bench.py run into a short text report.
+
+    python -m paper_2606_25473_amd.profile_summary --trace DIR [--fetch DIR --write DIR]
+        [--copy-mib N] [--workload NAME] [--op jvp|fwd] [--record profiles/hbm_traffic.json]
+
+--trace: a ``rocprofv3 --kernel-trace --stats -f csv`` output directory;
+--fetch/--write: ``rocprofv3 --pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE`` output
+directories of a bench run that also did ``--copy-calibration-mib N``.  The
+copy kernel of N MiB (N MiB read, N MiB written) calibrates the counters: the
+attention kernel's bytes = its counter value x (N MiB / the copy's counter).
+With --record, the per-launch HBM bytes are stored for bench.py together with
+a hash of the kernel sources (bench.py ignores the record once they change).
+"""
+import argparse
+import csv
+import glob
+import json
+import os
+import statistics
+
+ATTN = "attn_mfma_kernel"
+
+
+def _rows(d, suffix):
+    out = []
+    for f in glob.glob(os.path.join(d, "**", f"*{suffix}"), recursive=True):
+        with open(f, newline="") as fh:
+            out.extend(csv.DictReader(fh))
+    return out
+
+
+def kernel_stats(d):
+    rows = _rows(d, "kernel_stats.csv")
+    return [(r["Name"], int(r["Calls"]), float(r["AverageNs"]), float(r["MinNs"]), float(r["MaxNs"]),
+             float(r.get("Percentage", 0) or 0)) for r in rows]
+
+
+def counter_per_dispatch(d, counter):
+    """{kernel name: [value per dispatch]} for one counter."""
+    res = {}
+    for r in _rows(d, "counter_collection.csv"):
+        if r.get("Counter_Name") != counter:
+            continue
+        res.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+    return res
+
+
+def _pick(d, key):
+    for name, vals in d.items():
+        if key in name:
+            return name, vals
+    return None, []
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--trace")
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--copy-mib", type=int, default=0)
+    ap.add_argument("--workload", default="wan1.3b_chunkwise_tf")
+    ap.add_argument("--op", default="jvp", choices=["jvp", "fwd"])
+    ap.add_argument("--record")
+    a = ap.parse_args(argv)
+    lines = []
+    if a.trace:
+        st = sorted(kernel_stats(a.trace), key=lambda r: -r[2] * r[1])
+        lines.append("| kernel | calls | avg ms | min ms | max ms | % time |")
+        lines.append("|---|---|---|---|---|---|")
+        for name, calls, avg, mn, mx, pct in st[:8]:
+            lines.append(f"| {name[:90]} | {calls} | {avg / 1e6:.4f} | {mn / 1e6:.4f} | {mx / 1e6:.4f} | {pct:.1f} |")
+    traffic = None
+    if a.fetch and a.write and a.copy_mib:
+        nbytes = a.copy_mib * (1 << 20)
+        out = {}
+        for label, d, cnt in (("read", a.fetch, "FETCH_SIZE"), ("write", a.write, "WRITE_SIZE")):
+            per = counter_per_dispatch(d, cnt)
+            # the calibration copy is a device-to-device hipMemcpy (runtime blit kernel)
+            cname, cvals = _pick(per, "copyBuffer")
+            kname, kvals = _pick(per, ATTN)
+            if not cvals or not kvals:
+                lines.append(f"{cnt}: copy or attention kernel missing in {d}")
+                continue
+            copy_kib = max(cvals)          # the largest blit is the calibration copy
+            factor = nbytes / copy_kib      # bytes per counter unit
+            att = statistics.median(kvals) * factor
+            out[label] = att
+            lines.append(f"{cnt}: copy kernel `{cname[:60]}` {copy_kib:.0f} units for {nbytes} B "
+                         f"-> {factor:.1f} B/unit; attention kernel median {statistics.median(kvals):.0f} "
+                         f"units/dispatch over {len(kvals)} dispatches = {att / 1e9:.3f} GB")
+        if len(out) == 2:
+            traffic = out["read"] + out["write"]
+            lines.append(f"HBM traffic per launch: {traffic / 1e9:.3f} GB "
+                         f"(read {out['read'] / 1e9:.3f} + write {out['write'] / 1e9:.3f})")
+    print("\n".join(lines))
+    if a.record and traffic is not None:
+        import importlib.util
+        root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+        spec = importlib.util.spec_from_file_location("bench", os.path.join(root, "bench.py"))
+        bench = importlib.util.module_from_spec(spec)
+        spec.loader.exec_module(bench)
+        rec = {}
+        if os.path.exists(a.record):
+            with open(a.record) as f:
+                rec = json.load(f)
+        rec[f"{a.workload}:{a.op}"] = {"hbm_bytes_per_launch": traffic,
+                                       "kernel_source_hash": bench.kernel_source_hash()}
+        with open(a.record, "w") as f:
+            json.dump(rec, f, indent=1, sort_keys=True)
+
+
+if __name__ == "__main__":
+    main()
