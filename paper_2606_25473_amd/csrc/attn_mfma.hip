@@ -1,6 +1,6 @@
 // attn_mfma.hip -- bf16 masked attention forward + JVP on gfx950 matrix cores.
 //
-// One work-group of 4 waves owns a query tile of 128 rows (32 per wave) of one
+// One work-group of 8 waves owns a query tile of 256 rows (32 per wave) of one
 // (batch, head) and streams the key blocks of its plan (schedule.hpp) through
 // LDS, 32 keys at a time, with the online-softmax recurrence of the paper's
 // Algorithm 1 (App. B): running max m, normaliser l, the primal accumulator O,
@@ -52,7 +52,8 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int BR = kMfmaBr;
 constexpr int BC = kMfmaBc;
-constexpr int NTHREADS = 256;
+constexpr int NW = BR / 32;            // waves per work-group, 32 query rows each
+constexpr int NTHREADS = 64 * NW;
 constexpr float kLazy = 8.0f;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -64,9 +65,8 @@ struct Geo {
   static constexpr int TILEB = BC * ROWB;         // bytes per LDS tile of BC keys
   static constexpr int DT = D / 32;               // 32-wide d tiles of O^T / T^T
   static constexpr int KS = D / 16;               // 16-deep k steps of the score contraction
-  static constexpr int CPT = BC * NCH;            // chunks per tile
-  static constexpr int CPTH = CPT / NTHREADS;     // chunks per thread per tile
-  static_assert(CPT % NTHREADS == 0, "tile must split evenly over the work-group");
+  static constexpr int IPT = TILEB / 1024;        // 1 KiB direct-load instructions per key tile
+  static constexpr int IPQ = BR * ROWB / 1024;    // ... per query tile
 };
 
 // XOR swizzle of 16-byte chunks within an LDS row: conflict-free both for the
@@ -99,16 +99,20 @@ __device__ __forceinline__ bf16x8 cat(bf16x4 a, bf16x4 b) {
 __device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32, 64); }
 
 template <int D, bool JVP>
-__global__ __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_mfma_kernel(const AttnArgs a) {
   using G = Geo<D>;
   constexpr int TB = G::TILEB;
-  constexpr int TBJ = JVP ? G::TILEB : 16;  // tangent tiles exist only in the JVP kernel
+  constexpr int TBJ = JVP ? G::TILEB : 16;      // tangent tiles exist only in the JVP kernel
+  constexpr int QB = JVP ? BR * G::ROWB : 16;   // dQ tile (JVP only)
   // Two pipeline stages, each tile its own LDS object: the compiler then knows that
   // the loads streaming into one stage never alias the reads of the other, and does
-  // not wait for the prefetch before reading the current stage.
+  // not wait for the prefetch before reading the current stage.  dQ of the query tile
+  // lives in LDS too (read back as an MFMA operand), which keeps the per-wave register
+  // footprint within two waves per SIMD.
   __shared__ __attribute__((aligned(1024))) char sK0[TB], sV0[TB], sK1[TB], sV1[TB];
   __shared__ __attribute__((aligned(1024))) char sdK0[TBJ], sdV0[TBJ], sdK1[TBJ], sdV1[TBJ];
+  __shared__ __attribute__((aligned(1024))) char sdQ[QB];
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -133,7 +137,8 @@ void attn_mfma_kernel(const AttnArgs a) {
   const int nblk = plan_num_blocks(plan);
 
   // ---- this lane's query row and its admissible key ranges
-  const int row = q0 + wave * 32 + (lane & 31);
+  const int qrow = wave * 32 + (lane & 31);   // row within the tile
+  const int row = q0 + qrow;
   int ra0 = 0, ra1 = 0, rb0 = 0, rb1 = 0;
   for (int g = plan.g_first; g <= plan.g_last; ++g) {
     if (row >= group_q_begin(a.gt, g) && row < a.gt.q_end[g]) {
@@ -141,40 +146,35 @@ void attn_mfma_kernel(const AttnArgs a) {
     }
   }
 
-  // ---- Q^T / dQ^T as B operands: lane l holds row l%32, d = 16 s + 8 (l/32) + 0..7
-  bf16x8 qop[G::KS], dqop[JVP ? G::KS : 1];
+  // ---- Q^T as B operand in registers: lane l holds row l%32, d = 16 s + 8 (l/32) + 0..7
+  bf16x8 qop[G::KS];
 #pragma unroll
   for (int s = 0; s < G::KS; ++s) {
     // rows past the end are clamped to the last row (their outputs are not stored)
-    const size_t qoff = (size_t)min(row, L - 1) * D + 16 * s + 8 * hh;
-    qop[s] = *(const bf16x8*)(Qg + qoff);
-    if constexpr (JVP) dqop[s] = *(const bf16x8*)(dQg + qoff);
+    qop[s] = *(const bf16x8*)(Qg + (size_t)min(row, L - 1) * D + 16 * s + 8 * hh);
   }
 
-  // ---- global -> LDS staging of one key block: direct loads (global_load_lds_dwordx4).
-  // One wave instruction writes 64 lanes x 16 bytes = 1 KiB of consecutive LDS, i.e.
-  // 1024 / ROWB rows; the XOR swizzle is realised by choosing which logical chunk
-  // each lane fetches.  Keys past the end of the sequence are clamped to the last
-  // key (finite data; those keys are masked out of the softmax).
-  constexpr int IPT = G::TILEB / 1024;        // wave instructions per tile
-  constexpr int IPW = IPT / 4;                // per wave (4 waves)
-  static_assert(IPT % 4 == 0, "tile must split evenly over the 4 waves");
-  int dma_row[IPW], dma_col[IPW];
-#pragma unroll
-  for (int j = 0; j < IPW; ++j) {
-    const int byte = (wave * IPW + j) * 1024 + lane * 16;
-    const int r = byte / G::ROWB;
-    const int phys = (byte % G::ROWB) >> 4;
-    dma_row[j] = r;
-    dma_col[j] = (phys ^ swz<D>(r)) * 8;
-  }
+  // ---- global -> LDS staging: direct loads (global_load_lds_dwordx4).  One wave
+  // instruction writes 64 lanes x 16 bytes = 1 KiB of consecutive LDS, i.e. 1024 / ROWB
+  // rows; the XOR swizzle is realised by choosing which logical chunk each lane fetches.
+  // Rows past the end of the sequence are clamped to the last row (finite data; masked
+  // keys / unstored queries).
+  constexpr int RPI = 1024 / G::ROWB;  // rows per instruction
+  const int dma_r = (lane * 16) / G::ROWB;
+  const int dma_phys = ((lane * 16) % G::ROWB) >> 4;
+  auto dma_rows = [&](const bf16_t* src, int row0, int r, char* dst) {
+    const int rr = r + dma_r;
+    const int grow = min(row0 + rr, L - 1);
+    __builtin_amdgcn_global_load_lds(
+        (const __attribute__((address_space(1))) void*)(src + (size_t)grow * D + (dma_phys ^ swz<D>(rr)) * 8),
+        (__attribute__((address_space(3))) void*)(dst + r * G::ROWB), 16, 0, 0);
+  };
+  // one key tile of BC rows: instruction j (rows j*RPI ...) is issued by wave j % NW
   auto dma_tile = [&](const bf16_t* src, int k0, char* dst) {
 #pragma unroll
-    for (int j = 0; j < IPW; ++j) {
-      const int key = min(k0 + dma_row[j], L - 1);
-      __builtin_amdgcn_global_load_lds(
-          (const __attribute__((address_space(1))) void*)(src + (size_t)key * D + dma_col[j]),
-          (__attribute__((address_space(3))) void*)(dst + (wave * IPW + j) * 1024), 16, 0, 0);
+    for (int j0 = 0; j0 < G::IPT; j0 += NW) {
+      const int j = j0 + wave;
+      if (G::IPT % NW == 0 || j < G::IPT) dma_rows(src, k0, j * RPI, dst);
     }
   };
   auto dma_block = [&](int kb, char* k, char* v, char* dk, char* dv) {
@@ -235,8 +235,9 @@ void attn_mfma_kernel(const AttnArgs a) {
       S = mfma(kop, qop[s], S);
       if constexpr (JVP) {
         const bf16x8 dkop = *(const bf16x8*)(cdK + off);
+        const bf16x8 dqop = *(const bf16x8*)(sdQ + lds_off<D>(qrow, 2 * s + hh));
         dS = mfma(dkop, qop[s], dS);
-        dS = mfma(kop, dqop[s], dS);
+        dS = mfma(kop, dqop, dS);
       }
     }
 
@@ -309,6 +310,11 @@ void attn_mfma_kernel(const AttnArgs a) {
     return false;
   };
 
+  // prologue: dQ of the query tile, then the first key block
+  if constexpr (JVP) {
+#pragma unroll
+    for (int j0 = 0; j0 < G::IPQ; j0 += NW) dma_rows(dQg, q0, (j0 + wave) * RPI, sdQ);
+  }
   if (nblk > 0) dma_block(plan_block(plan, 0), sK0, sV0, sdK0, sdV0);
   __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): this wave's LDS loads have landed
   __syncthreads();

@@ -25,8 +25,8 @@ struct AttnArgs {
   TileOrder order;
 };
 
-// bf16 MFMA kernels: query tiles of kMfmaBr rows (4 waves x 32 rows), key blocks of kMfmaBc keys.
-constexpr int kMfmaBr = 128;
+// bf16 MFMA kernels: query tiles of kMfmaBr rows (8 waves x 32 rows), key blocks of kMfmaBc keys.
+constexpr int kMfmaBr = 256;
 constexpr int kMfmaBc = 32;
 
 // fp32 exact-path kernels: one wave per query row.

@@ -61,6 +61,7 @@ def main(argv=None):
     ap.add_argument("--workload", default="wan1.3b_chunkwise_tf")
     ap.add_argument("--op", default="jvp", choices=["jvp", "fwd"])
     ap.add_argument("--record")
+    ap.add_argument("--pmc", nargs="*", default=[], help="counter-collection output dirs to list")
     a = ap.parse_args(argv)
     lines = []
     if a.trace:
@@ -92,6 +93,13 @@ def main(argv=None):
             traffic = out["read"] + out["write"]
             lines.append(f"HBM traffic per launch: {traffic / 1e9:.3f} GB "
                          f"(read {out['read'] / 1e9:.3f} + write {out['write'] / 1e9:.3f})")
+    for d in a.pmc:
+        per = {}
+        for r in _rows(d, "counter_collection.csv"):
+            if ATTN in r["Kernel_Name"]:
+                per.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+        for cnt in sorted(per):
+            lines.append(f"{cnt}: median {statistics.median(per[cnt]):.6g} per dispatch ({len(per[cnt])} dispatches)")
     print("\n".join(lines))
     if a.record and traffic is not None:
         import importlib.util
