@@ -162,11 +162,13 @@ void attn_mfma_kernel(const AttnArgs a) {
   constexpr int RPI = 1024 / G::ROWB;  // rows per instruction
   const int dma_r = (lane * 16) / G::ROWB;
   const int dma_phys = ((lane * 16) % G::ROWB) >> 4;
+  // (uniform 64-bit base + 32-bit per-lane byte offset: one head is < 4 GiB)
   auto dma_rows = [&](const bf16_t* src, int row0, int r, char* dst) {
     const int rr = r + dma_r;
-    const int grow = min(row0 + rr, L - 1);
+    const unsigned grow = (unsigned)min(row0 + rr, L - 1);
+    const unsigned off = (grow * D + (unsigned)((dma_phys ^ swz<D>(rr)) * 8)) * 2u;
     __builtin_amdgcn_global_load_lds(
-        (const __attribute__((address_space(1))) void*)(src + (size_t)grow * D + (dma_phys ^ swz<D>(rr)) * 8),
+        (const __attribute__((address_space(1))) void*)((const char*)src + off),
         (__attribute__((address_space(3))) void*)(dst + r * G::ROWB), 16, 0, 0);
   };
   // one key tile of BC rows: instruction j (rows j*RPI ...) is issued by wave j % NW
