@@ -98,6 +98,30 @@ __device__ __forceinline__ bf16x8 cat(bf16x4 a, bf16x4 b) {
 
 __device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32, 64); }
 
+// Direct global -> LDS load of 16 bytes per lane (global_load_lds_dwordx4): lane l's
+// bytes land at LDS address lds + 16 l.  Issued from inline assembly on purpose: the
+// compiler then does not track these loads, so it never inserts waits for them before
+// LDS reads of other pipeline stages (it cannot tell stages apart when the stage index
+// is a run-time value).  The kernel waits for them itself (vmcnt) before a barrier.
+// M0 carries the LDS base address (one wait state separates its write from the load);
+// M0 is saved and restored around the load because the compiler reserves it.
+__device__ __forceinline__ void lds_load16(const void* gbase, unsigned byte_off, unsigned lds) {
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(byte_off), "s"(gbase), "s"(__builtin_amdgcn_readfirstlane(lds))
+      : "memory");
+}
+
+__device__ __forceinline__ unsigned lds_addr(const void* p) {
+  return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
 template <int D, bool JVP>
 __global__ __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_mfma_kernel(const AttnArgs a) {
@@ -105,17 +129,17 @@ void attn_mfma_kernel(const AttnArgs a) {
   constexpr int TB = G::TILEB;
   constexpr int TBJ = JVP ? G::TILEB : 16;      // tangent tiles exist only in the JVP kernel
   constexpr int QB = JVP ? BR * G::ROWB : 16;   // dQ tile (JVP only)
-  // Two pipeline stages, each tile its own LDS object: the compiler then knows that
-  // the loads streaming into one stage never alias the reads of the other, and does
-  // not wait for the prefetch before reading the current stage.  dQ of the query tile
-  // lives in LDS too (read back as an MFMA operand), which keeps the per-wave register
-  // footprint within two waves per SIMD.
-  __shared__ __attribute__((aligned(1024))) char sK0[TB], sV0[TB], sK1[TB], sV1[TB];
-  __shared__ __attribute__((aligned(1024))) char sdK0[TBJ], sdV0[TBJ], sdK1[TBJ], sdV1[TBJ];
+  // Three pipeline stages (block k is read from stage k mod 3 while block k+2 streams
+  // into stage (k+2) mod 3), each holding the K, V, dK, dV tiles of one key block.
+  // dQ of the query tile lives in LDS too (read back as an MFMA operand), which keeps
+  // the per-wave register footprint within two waves per SIMD.
+  // D = 128 JVP: 3 x 32 KiB + 64 KiB = 160 KiB.
+  constexpr int SB = 2 * TB + 2 * TBJ;
+  __shared__ __attribute__((aligned(1024))) char stages[3 * SB];
   __shared__ __attribute__((aligned(1024))) char sdQ[QB];
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int lane = tid & 63;
   const int hh = lane >> 5;   // which half of the wave (key sub-block within S^T)
   const int L = a.L;
@@ -163,29 +187,29 @@ void attn_mfma_kernel(const AttnArgs a) {
   const int dma_r = (lane * 16) / G::ROWB;
   const int dma_phys = ((lane * 16) % G::ROWB) >> 4;
   // (uniform 64-bit base + 32-bit per-lane byte offset: one head is < 4 GiB)
-  auto dma_rows = [&](const bf16_t* src, int row0, int r, char* dst) {
+  // LDS destinations are passed as byte addresses (uniform integers)
+  auto dma_rows = [&](const bf16_t* src, int row0, int r, unsigned dst) {
     const int rr = r + dma_r;
     const unsigned grow = (unsigned)min(row0 + rr, L - 1);
     const unsigned off = (grow * D + (unsigned)((dma_phys ^ swz<D>(rr)) * 8)) * 2u;
-    __builtin_amdgcn_global_load_lds(
-        (const __attribute__((address_space(1))) void*)((const char*)src + off),
-        (__attribute__((address_space(3))) void*)(dst + r * G::ROWB), 16, 0, 0);
+    lds_load16(src, off, dst + (unsigned)(r * G::ROWB));
   };
   // one key tile of BC rows: instruction j (rows j*RPI ...) is issued by wave j % NW
-  auto dma_tile = [&](const bf16_t* src, int k0, char* dst) {
+  auto dma_tile = [&](const bf16_t* src, int k0, unsigned dst) {
 #pragma unroll
     for (int j0 = 0; j0 < G::IPT; j0 += NW) {
       const int j = j0 + wave;
       if (G::IPT % NW == 0 || j < G::IPT) dma_rows(src, k0, j * RPI, dst);
     }
   };
-  auto dma_block = [&](int kb, char* k, char* v, char* dk, char* dv) {
+  // the K, V, dK, dV tiles of key block kb into the stage at LDS address st
+  auto dma_block = [&](int kb, unsigned st) {
     const int k0 = kb * BC;
-    dma_tile(Kg, k0, k);
-    dma_tile(Vg, k0, v);
+    dma_tile(Kg, k0, st);
+    dma_tile(Vg, k0, st + TB);
     if constexpr (JVP) {
-      dma_tile(dKg, k0, dk);
-      dma_tile(dVg, k0, dv);
+      dma_tile(dKg, k0, st + 2 * TB);
+      dma_tile(dVg, k0, st + 2 * TB + TBJ);
     }
   };
 
@@ -219,13 +243,25 @@ void attn_mfma_kernel(const AttnArgs a) {
   const float sc = a.scale;
   const int krow = lane & 31;
 
+  // End of an iteration: wait until every load but this iteration's prefetch (N per
+  // wave) has landed -- so the next block is complete -- and every LDS read has
+  // returned, then synchronise the work-group.  D = 128: every wave issues one load per
+  // tile; D = 64: waves 0..3 do and the others issue none (nothing outstanding).
+  auto end_iteration = [&]() {
+    constexpr int N = (JVP ? 4 : 2) * ((G::IPT + NW - 1) / NW);
+    static_assert(N == 2 || N == 4, "vmcnt immediate below");
+    if constexpr (N == 4) asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(2) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  };
+
   // One key block.  Returns true -- before touching any accumulator -- if some row's
   // block max exceeds its reference by more than kLazy; the caller then rescales and
   // redoes the block.
   auto step = [&](int it, const char* cK, const char* cV, const char* cdK, const char* cdV,
-                  char* nK, char* nV, char* ndK, char* ndV) -> bool {
-    // prefetch the next block into the other stage (free since the last barrier)
-    if (it + 1 < nblk) dma_block(plan_block(plan, it + 1), nK, nV, ndK, ndV);
+                  unsigned next_stage) -> bool {
+    // prefetch block it+2 into the stage freed by block it-1: a fixed number of loads
+    // per iteration (indices past the end are clamped; that stage is never read)
+    dma_block(plan_block(plan, min(it + 2, nblk - 1)), next_stage);
     const int k0 = plan_block(plan, it) * BC;
 
     // ---- scores and score tangents (transposed): S^T = K Q^T, dS^T = dK Q^T + K dQ^T
@@ -307,39 +343,43 @@ void attn_mfma_kernel(const AttnArgs a) {
       }
     }
 
-    __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): the prefetch into the other stage has landed
-    __syncthreads();                    // ... for every wave, and nobody reads this stage any more
+    end_iteration();  // block it+1 is in for every wave; nobody reads stage `it` any more
     return false;
   };
 
-  // prologue: dQ of the query tile, then the first key block
+  // prologue: dQ of the query tile, then the first two key blocks
+  const unsigned st_lds = __builtin_amdgcn_readfirstlane(lds_addr(stages));
   if constexpr (JVP) {
+    const unsigned dq_lds = __builtin_amdgcn_readfirstlane(lds_addr(sdQ));
 #pragma unroll
-    for (int j0 = 0; j0 < G::IPQ; j0 += NW) dma_rows(dQg, q0, (j0 + wave) * RPI, sdQ);
+    for (int j0 = 0; j0 < G::IPQ; j0 += NW) dma_rows(dQg, q0, (j0 + wave) * RPI, dq_lds);
   }
-  if (nblk > 0) dma_block(plan_block(plan, 0), sK0, sV0, sdK0, sdV0);
-  __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): this wave's LDS loads have landed
+  if (nblk > 0) {
+    dma_block(plan_block(plan, 0), st_lds);
+    dma_block(plan_block(plan, min(1, nblk - 1)), st_lds + SB);
+  }
+  // vmcnt(0) through the builtin, so that the compiler also knows that the Q operand
+  // loads above are complete and does not wait for them inside the loop
+  __builtin_amdgcn_s_waitcnt(0xF70);
   __syncthreads();
 
   int it = 0;
+  int cur = 0;  // stage of block it
   while (it < nblk) {
-    // hot loop, unrolled by two so that every LDS access names its stage statically
     bool rescale = false;
-    if (it & 1) {
-      rescale = step(it, sK1, sV1, sdK1, sdV1, sK0, sV0, sdK0, sdV0);
-      if (!rescale) ++it;
-    }
-    while (!rescale && it < nblk) {
-      rescale = step(it, sK0, sV0, sdK0, sdV0, sK1, sV1, sdK1, sdV1);
-      if (rescale || ++it >= nblk) break;
-      rescale = step(it, sK1, sV1, sdK1, sdV1, sK0, sV0, sdK0, sdV0);
-      if (!rescale) ++it;
+    while (it < nblk) {
+      const int nxt = cur == 0 ? 2 : cur - 1;  // (it + 2) mod 3
+      const char* cs = stages + cur * SB;
+      rescale = step(it, cs, cs + TB, cs + 2 * TB, cs + 2 * TB + TBJ, st_lds + (unsigned)(nxt * SB));
+      if (rescale) break;
+      ++it;
+      cur = cur == 2 ? 0 : cur + 1;
     }
     if (!rescale) break;
     // Cold path: move the reference max of the rows that need it (lanes l and l^32 hold
     // the same query, so the new reference is their joint max), rescale O, T, l, r, and
-    // redo block `it` (its S is recomputed; the stage still holds its K/V, and the
-    // repeated prefetch rewrites the other stage with identical data).
+    // redo block `it` (its S is recomputed; its stage still holds its K/V, and the
+    // repeated prefetch rewrites stage (it+2) mod 3 with identical data).
     const float mx = fmaxf(mpend, xor32(mpend));
     const bool up = mx > m + kLazy;
     const float mnew = up ? mx : m;
@@ -353,6 +393,8 @@ void attn_mfma_kernel(const AttnArgs a) {
     }
     m = mnew;
   }
+
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the clamped tail prefetches have landed
 
   // ---- epilogue: combine the two half-waves' partial sums, normalise, store
   const float l_tot = lsum + xor32(lsum);
