@@ -93,13 +93,32 @@ def main(argv=None):
             traffic = out["read"] + out["write"]
             lines.append(f"HBM traffic per launch: {traffic / 1e9:.3f} GB "
                          f"(read {out['read'] / 1e9:.3f} + write {out['write'] / 1e9:.3f})")
+    derived = {}
     for d in a.pmc:
-        per = {}
+        per, dur = {}, []
         for r in _rows(d, "counter_collection.csv"):
             if ATTN in r["Kernel_Name"]:
                 per.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+                if r["Counter_Name"] == "GRBM_GUI_ACTIVE":
+                    dur.append(float(r["End_Timestamp"]) - float(r["Start_Timestamp"]))
+        xcc = 8
+        for info in _rows(d, "agent_info.csv"):
+            if info.get("Num_Xcc", "0") not in ("", "0"):
+                xcc = int(info["Num_Xcc"])
         for cnt in sorted(per):
             lines.append(f"{cnt}: median {statistics.median(per[cnt]):.6g} per dispatch ({len(per[cnt])} dispatches)")
+        if "GRBM_GUI_ACTIVE" in per and dur:
+            # the counter is summed over the XCDs; per-XCD cycles / dispatch time = shader clock
+            cyc = statistics.median(per["GRBM_GUI_ACTIVE"]) / xcc
+            derived["clock_ghz"] = cyc / statistics.median(dur)
+            lines.append(f"shader clock during the kernel: {derived['clock_ghz']:.3f} GHz "
+                         f"(GRBM_GUI_ACTIVE / {xcc} XCDs / dispatch time {statistics.median(dur) / 1e6:.3f} ms)")
+            if "SQ_VALU_MFMA_BUSY_CYCLES" in per:
+                simds = 1024
+                util = statistics.median(per["SQ_VALU_MFMA_BUSY_CYCLES"]) / (cyc * simds)
+                derived["mfma_busy"] = util
+                lines.append(f"MFMA busy: {100 * util:.1f} % of SIMD cycles "
+                             f"(SQ_VALU_MFMA_BUSY_CYCLES / (per-XCD GRBM_GUI_ACTIVE x {simds} SIMDs))")
     print("\n".join(lines))
     if a.record and traffic is not None:
         import importlib.util
@@ -111,8 +130,9 @@ def main(argv=None):
         if os.path.exists(a.record):
             with open(a.record) as f:
                 rec = json.load(f)
-        rec[f"{a.workload}:{a.op}"] = {"hbm_bytes_per_launch": traffic,
-                                       "kernel_source_hash": bench.kernel_source_hash()}
+        ent = {"hbm_bytes_per_launch": traffic, "kernel_source_hash": bench.kernel_source_hash()}
+        ent.update(derived)
+        rec[f"{a.workload}:{a.op}"] = ent
         with open(a.record, "w") as f:
             json.dump(rec, f, indent=1, sort_keys=True)
 
