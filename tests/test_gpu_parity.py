@@ -206,3 +206,44 @@ def test_full_size_sampled_rows(name):
                   _rel(_np(fwd[1][b, h].index_select(0, ridx)), LSE[0, 0]))
             _say(f"[full-size] {name} attn_fwd (b={b}, h={h}) rel-L2 O={ef[0]:.3e} LSE={ef[1]:.3e}")
             assert max(ef) <= TOL["bf16"], ef
+
+
+# ----------------------------------------------------------------------------- rescale stress
+
+def _scaled_inputs(w, seed, key_gain):
+    """Inputs whose key norms grow along the sequence (gain per key position), so that
+    the running row maximum keeps increasing and the reference max must move often."""
+    x = make_inputs(w, "cpu", seed)
+    L = w.L
+    g = torch.exp(torch.linspace(0.0, float(np.log(key_gain)), L))[None, None, :, None]
+    for k in ("K", "dK"):
+        x[k] = (x[k].float() * g).to(x[k].dtype)
+    return x
+
+
+@pytest.mark.parametrize("dt,gain,qscale", [("bf16", 12.0, 1.0), ("bf16", 3.0, 4.0), ("f32", 12.0, 1.0)])
+def test_growing_scores_force_rescales(dt, gain, qscale):
+    """Scores rise along the keys (up to ~gain x), so blocks keep exceeding the stored
+    reference max: exercises the rescale path on every kind of row and block."""
+    w = custom_workload(f"rescale_{dt}_{gain}_{qscale}", 1, 2, 128, dt, MASK_TEACHER_FORCING, 3, 130,
+                        tangent_std=0.5)
+    _say(f"[rescale] {w.name}")
+    x = _scaled_inputs(w, 8, gain)
+    x["Q"] = (x["Q"].float() * qscale).to(x["Q"].dtype)
+    o, do, lse = _run_gpu(w, x)
+    O, dO, LSE = attention_jvp(*[_np(x[k]) for k in ("Q", "K", "V", "dQ", "dK", "dV")], w.kind, _offsets(w))
+    errs = (_rel(_np(o), O), _rel(_np(do), dO), _rel(_np(lse), LSE))
+    _say(f"[rescale] {w.name} rel-L2 O={errs[0]:.3e} dO={errs[1]:.3e} LSE={errs[2]:.3e}")
+    assert np.isfinite(_np(o)).all() and np.isfinite(_np(do)).all()
+    assert max(errs) <= TOL[dt], errs
+
+
+def test_full_mask_growing_scores():
+    w = custom_workload("rescale_full_bf16", 1, 1, 128, "bf16", MASK_FULL, L=777, tangent_std=0.5)
+    _say("[rescale] full mask, growing key norms")
+    x = _scaled_inputs(w, 9, 20.0)
+    o, do, lse = _run_gpu(w, x)
+    O, dO, LSE = attention_jvp(*[_np(x[k]) for k in ("Q", "K", "V", "dQ", "dK", "dV")], w.kind, None)
+    errs = (_rel(_np(o), O), _rel(_np(do), dO), _rel(_np(lse), LSE))
+    _say(f"[rescale] full rel-L2 O={errs[0]:.3e} dO={errs[1]:.3e} LSE={errs[2]:.3e}")
+    assert max(errs) <= TOL["bf16"], errs
