@@ -42,19 +42,19 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload, forward):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel source; else None."""
+def profile_record(workload, forward):
+    """The committed rocprofv3 counter record of this workload (HBM bytes per launch,
+    shader clock, MFMA busy fraction), if it was taken on the current kernel source;
+    else an empty dict."""
     path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     if not os.path.exists(path):
-        return None
+        return {}
     with open(path) as f:
         rec = json.load(f)
-    key = f"{workload}:{'fwd' if forward else 'jvp'}"
-    ent = rec.get(key)
+    ent = rec.get(f"{workload}:{'fwd' if forward else 'jvp'}")
     if not ent or ent.get("kernel_source_hash") != kernel_source_hash():
-        return None
-    return ent.get("hbm_bytes_per_launch")
+        return {}
+    return ent
 
 
 def cpu_baseline(w, x, out, forward, budget_s=15.0):
@@ -170,7 +170,8 @@ def main():
     value = flop / (ms_per_step * 1e-3) / 1e12
     achieved = flop / (kernel_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_TFLOPS
-    traffic = measured_traffic(w.name, args.forward)
+    prof = profile_record(w.name, args.forward)
+    traffic = prof.get("hbm_bytes_per_launch")
     res = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -187,12 +188,19 @@ def main():
         "config": dict(w.describe(), op="attn_fwd" if args.forward else "attn_jvp_fwd"),
         "pct_peak": round(100 * achieved / peak, 2),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": round(peak, 1),
-                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": traffic},
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                     "traffic": None if traffic is None else round(traffic)},
         "kernel_ms": {"mean": round(kernel_ms, 4), "median": round(float(np.median(per)), 4),
                       "min": round(min(per), 4)},
         "unmasked_pairs_per_head": pairs,
         "computed_over_unmasked": round(computed / pairs, 4),
     }
+    if prof.get("clock_ghz"):
+        # the nominal peak assumes 2.4 GHz; under this load the shader clock is lower
+        clk = prof["clock_ghz"]
+        res["roofline"]["measured_clock_ghz"] = round(clk, 3)
+        res["roofline"]["frac_at_measured_clock"] = round(achieved / (peak * clk / 2.4), 4)
+        res["roofline"]["mfma_busy_cycles_frac"] = round(prof.get("mfma_busy", 0.0), 4)
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(w, x, (o, do, lse), args.forward, args.cpu_budget)
     print(json.dumps(res), flush=True)
