@@ -56,7 +56,8 @@ enum {
 enum {
   ATTN_MASK_FULL = 0,             /* every query sees every key; num_chunks/offsets ignored */
   ATTN_MASK_BLOCK_CAUSAL = 1,     /* query in chunk i sees chunks <= i; requires L == o_N */
-  ATTN_MASK_TEACHER_FORCING = 2   /* [clean c_1..c_N | noisy c_1..c_N]; requires L == 2 o_N */
+  ATTN_MASK_TEACHER_FORCING = 2,  /* [clean c_1..c_N | noisy c_1..c_N]; requires L == 2 o_N */
+  ATTN_MASK_RANGES = 3            /* explicit query groups with key ranges (see attn_chunk_layout) */
 };
 
 enum {
@@ -69,15 +70,27 @@ enum {
 /* largest number of chunks a layout may have (the derived query-group table
  * travels in the kernel arguments, so its size is bounded) */
 #define ATTN_MAX_CHUNKS 64
+/* largest number of query groups of an ATTN_MASK_RANGES layout */
+#define ATTN_MAX_GROUPS 128
 
 /* Chunk layout of the mask.  chunk_offsets (HOST memory) holds num_chunks + 1
  * strictly increasing prefix offsets 0 = o_0 < o_1 < ... < o_N of the chunk
  * boundaries within ONE half of the TF sequence (teacher forcing) or within the
- * sequence (block-causal).  Uniform chunks of C tokens use o_i = i * C. */
+ * sequence (block-causal).  Uniform chunks of C tokens use o_i = i * C.
+ *
+ * ATTN_MASK_RANGES gives the query-group / key-range representation directly (paper
+ * App. B, "Sparse custom-mask representation"): num_chunks = G query groups
+ * (1..ATTN_MAX_GROUPS) and `ranges` (HOST memory) holds 5 G ints, per group
+ * q_end, a0, a1, b0, b1: group g owns query rows [q_end(g-1), q_end(g)) (q_end(-1) = 0,
+ * strictly increasing, q_end(G-1) = L) and admits keys in [a0, a1) and [b0, b1)
+ * (0 <= begin <= end <= L; an empty range has begin == end; the two ranges must not
+ * overlap).  A group with two empty ranges has fully masked rows: O = 0, dO = 0,
+ * LSE = -inf. */
 typedef struct attn_chunk_layout {
   int32_t kind;                  /* ATTN_MASK_* */
-  int32_t num_chunks;            /* N, 1..ATTN_MAX_CHUNKS (ignored for FULL) */
-  const int32_t* chunk_offsets;  /* N + 1 host ints (ignored for FULL, may be NULL) */
+  int32_t num_chunks;            /* N (chunks) or G (groups, ATTN_MASK_RANGES); ignored for FULL */
+  const int32_t* chunk_offsets;  /* N + 1 host ints (block-causal / TF only; else may be NULL) */
+  const int32_t* ranges;         /* 5 G host ints (ATTN_MASK_RANGES only; else may be NULL) */
 } attn_chunk_layout;
 
 /* Fused masked attention forward + JVP (paper App. B, Algorithm 1).

@@ -8,7 +8,8 @@ it, and this package imports nothing from the product.
 Contents
 --------
 masks      -- the attention mask materialised from its definition (per-token
-              chunk ids), for the full, block-causal and teacher-forcing kinds.
+              chunk ids), for the full, block-causal and teacher-forcing kinds,
+              and from an explicit query-group / key-range list.
 attention  -- closed-form masked attention O, LSE and the forward-mode tangent
               dO (paper, App. B, the masked-attention and tangent equations).
 dual       -- a pure-Python dual-number evaluation of the same map, used on
@@ -19,10 +20,10 @@ Parity status: every function here is pinned by tests in
 scaled_dot_product_attention and torch.func.jvp, the two-pass TF identity,
 hand-derived golden values and invariants).
 """
-from .masks import MASK_FULL, MASK_BLOCK_CAUSAL, MASK_TEACHER_FORCING, allowed_mask, count_allowed_pairs
+from .masks import MASK_FULL, MASK_BLOCK_CAUSAL, MASK_TEACHER_FORCING, MASK_RANGES, allowed_mask, count_allowed_pairs
 from .attention import attention_jvp, attention_fwd
 
 __all__ = [
-    "MASK_FULL", "MASK_BLOCK_CAUSAL", "MASK_TEACHER_FORCING",
+    "MASK_FULL", "MASK_BLOCK_CAUSAL", "MASK_TEACHER_FORCING", "MASK_RANGES",
     "allowed_mask", "count_allowed_pairs", "attention_jvp", "attention_fwd",
 ]

@@ -10,6 +10,11 @@ background section on TF / DF training):
                          A clean query in chunk j attends clean chunks <= j; a
                          noisy query in chunk i attends clean chunks < i and
                          the noisy chunk i itself (bidirectional inside it).
+* ``ranges``          -- the mask given directly as query groups with key ranges
+                         (paper App. B, sparse custom-mask representation): a list
+                         of (q_end, a0, a1, b0, b1); group g owns query rows
+                         [q_end of g-1, q_end) and admits keys in [a0, a1) and
+                         [b0, b1).  Passed in place of ``offsets``.
 
 A chunk layout is the prefix array ``offsets`` = [o_0=0 < o_1 < ... < o_N] of
 chunk boundaries within ONE half (TF) or within the whole sequence
@@ -21,6 +26,7 @@ import numpy as np
 MASK_FULL = "full"
 MASK_BLOCK_CAUSAL = "block_causal"
 MASK_TEACHER_FORCING = "teacher_forcing"
+MASK_RANGES = "ranges"
 
 
 def _chunk_of(tok, offsets):
@@ -33,6 +39,8 @@ def expected_length(kind, offsets):
     """Sequence length implied by a layout (None for the full mask)."""
     if kind == MASK_FULL:
         return None
+    if kind == MASK_RANGES:
+        return int(offsets[-1][0])
     half = int(offsets[-1])
     return 2 * half if kind == MASK_TEACHER_FORCING else half
 
@@ -43,6 +51,17 @@ def allowed_mask(kind, offsets, L, rows=None):
     cols = np.arange(L, dtype=np.int64)
     if kind == MASK_FULL:
         return np.ones((rows.size, L), dtype=bool)
+    if kind == MASK_RANGES:
+        groups = [tuple(int(v) for v in g) for g in offsets]
+        assert groups[-1][0] == L, "query groups must cover the sequence"
+        q_end = np.array([g[0] for g in groups])
+        g_of_row = np.searchsorted(q_end, rows, side="right")
+        out = np.zeros((rows.size, L), dtype=bool)
+        for i, g in enumerate(g_of_row):
+            _, a0, a1, b0, b1 = groups[g]
+            out[i, a0:a1] = True
+            out[i, b0:b1] = True
+        return out
     if kind == MASK_BLOCK_CAUSAL:
         assert L == int(offsets[-1]), "block-causal layout must cover the sequence"
         cq = _chunk_of(rows, offsets)[:, None]

@@ -14,7 +14,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 _LIBPATH = os.path.join(_PKG, "lib", "libattnjvp.so")
 
 DTYPE_F32, DTYPE_BF16 = 0, 1
-MASK_KINDS = {"full": 0, "block_causal": 1, "teacher_forcing": 2}
+MASK_KINDS = {"full": 0, "block_causal": 1, "teacher_forcing": 2, "ranges": 3}
 MAX_CHUNKS = 64
 ERR_NAMES = {1: "invalid argument", 2: "unsupported", 3: "HIP error"}
 
@@ -27,7 +27,8 @@ class AttnError(RuntimeError):
 
 class _Layout(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("num_chunks", ctypes.c_int32),
-                ("chunk_offsets", ctypes.POINTER(ctypes.c_int32))]
+                ("chunk_offsets", ctypes.POINTER(ctypes.c_int32)),
+                ("ranges", ctypes.POINTER(ctypes.c_int32))]
 
 
 _lib = None
@@ -72,11 +73,20 @@ def load_library():
 
 
 def make_layout(kind, offsets=None):
-    """C layout struct for mask ``kind`` ('full' | 'block_causal' | 'teacher_forcing' or its code)."""
+    """C layout struct for mask ``kind`` ('full' | 'block_causal' | 'teacher_forcing' |
+    'ranges', or its code).  ``offsets``: chunk prefix offsets, or for 'ranges' the
+    query groups [(q_end, a0, a1, b0, b1), ...]."""
     code = MASK_KINDS[kind] if isinstance(kind, str) else int(kind)
+    if code == MASK_KINDS["ranges"]:
+        groups = [tuple(int(v) for v in g) for g in (offsets or [])]
+        flat = [v for g in groups for v in g]
+        arr = (ctypes.c_int32 * max(1, len(flat)))(*flat)
+        lay = _Layout(code, len(groups), None, arr)
+        lay._keep = arr
+        return lay
     offs = [] if offsets is None else [int(x) for x in offsets]
     arr = (ctypes.c_int32 * max(1, len(offs)))(*offs) if offs else None
-    lay = _Layout(code, max(0, len(offs) - 1), arr if arr is not None else None)
+    lay = _Layout(code, max(0, len(offs) - 1), arr if arr is not None else None, None)
     lay._keep = arr  # keep the offsets array alive with the struct
     return lay
 

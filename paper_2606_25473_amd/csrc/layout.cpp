@@ -29,6 +29,28 @@ bool build_groups(const attn_chunk_layout* layout, int L, GroupTable* gt, std::s
     add_group(gt, L, 0, L, 0, 0);
     return true;
   }
+  if (kind == ATTN_MASK_RANGES) {
+    const int G = layout->num_chunks;
+    if (G < 1 || G > ATTN_MAX_GROUPS)
+      return fail(err, "number of query groups must be in [1, " + std::to_string(ATTN_MAX_GROUPS) +
+                           "], got " + std::to_string(G));
+    const int32_t* r = layout->ranges;
+    if (!r) return fail(err, "ranges is NULL");
+    int prev = 0;
+    for (int g = 0; g < G; ++g) {
+      const int qe = r[5 * g], a0 = r[5 * g + 1], a1 = r[5 * g + 2], b0 = r[5 * g + 3], b1 = r[5 * g + 4];
+      const std::string at = " (group " + std::to_string(g) + ")";
+      if (qe <= prev) return fail(err, "query group ends must be strictly increasing" + at);
+      if (a0 < 0 || a0 > a1 || a1 > L || b0 < 0 || b0 > b1 || b1 > L)
+        return fail(err, "key ranges must satisfy 0 <= begin <= end <= L" + at);
+      if (a1 > a0 && b1 > b0 && a0 < b1 && b0 < a1) return fail(err, "key ranges overlap" + at);
+      add_group(gt, qe, a0, a1, b0, b1);
+      prev = qe;
+    }
+    if (prev != L)
+      return fail(err, "query groups cover " + std::to_string(prev) + " rows but L = " + std::to_string(L));
+    return true;
+  }
   if (kind != ATTN_MASK_BLOCK_CAUSAL && kind != ATTN_MASK_TEACHER_FORCING)
     return fail(err, "unknown mask kind " + std::to_string(kind));
   const int N = layout->num_chunks;

@@ -30,7 +30,7 @@
 
 namespace attn {
 
-constexpr int kMaxGroups = 128;  // 2 * ATTN_MAX_CHUNKS
+constexpr int kMaxGroups = 128;  // 2 * ATTN_MAX_CHUNKS = ATTN_MAX_GROUPS
 
 struct GroupTable {
   int32_t n;

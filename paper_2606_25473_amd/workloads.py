@@ -20,6 +20,7 @@ import torch
 MASK_FULL = "full"
 MASK_BLOCK_CAUSAL = "block_causal"
 MASK_TEACHER_FORCING = "teacher_forcing"
+MASK_RANGES = "ranges"
 
 TOKENS_PER_LATENT_FRAME = 1560
 
@@ -32,7 +33,7 @@ class Workload:
     D: int
     dtype: str                 # "f32" or "bf16"
     kind: str                  # MASK_* above
-    offsets: tuple = field(default=())   # chunk prefix offsets within one half (TF) / the sequence
+    offsets: tuple = field(default=())   # chunk prefix offsets (TF / block-causal) or query groups (ranges)
     L_full: int = 0            # sequence length for the full mask
     tangent_std: float = 1.0
 
@@ -40,12 +41,14 @@ class Workload:
     def L(self) -> int:
         if self.kind == MASK_FULL:
             return self.L_full
+        if self.kind == MASK_RANGES:
+            return self.offsets[-1][0]
         half = self.offsets[-1]
         return 2 * half if self.kind == MASK_TEACHER_FORCING else half
 
     @property
     def num_chunks(self) -> int:
-        return max(0, len(self.offsets) - 1)
+        return len(self.offsets) if self.kind == MASK_RANGES else max(0, len(self.offsets) - 1)
 
     @property
     def torch_dtype(self):
@@ -54,7 +57,9 @@ class Workload:
     def describe(self) -> dict:
         d = {"workload": self.name, "B": self.B, "H": self.H, "L": self.L, "D": self.D,
              "dtype": self.dtype, "mask": self.kind}
-        if self.kind != MASK_FULL:
+        if self.kind == MASK_RANGES:
+            d["groups"] = len(self.offsets)
+        elif self.kind != MASK_FULL:
             sizes = sorted(set(self.offsets[i + 1] - self.offsets[i] for i in range(self.num_chunks)))
             d["chunks"] = self.num_chunks
             d["chunk_tokens"] = sizes[0] if len(sizes) == 1 else sizes
@@ -110,5 +115,7 @@ def custom_workload(name, B, H, D, dtype, kind, num_chunks=0, chunk=0, L=0, tang
     """A workload of arbitrary shape (tests: ragged tails, C=1, N=1, D=64 ...)."""
     if kind == MASK_FULL:
         return Workload(name, B, H, D, dtype, kind, (), L, tangent_std)
+    if kind == MASK_RANGES:
+        return Workload(name, B, H, D, dtype, kind, tuple(tuple(g) for g in offsets), 0, tangent_std)
     offs = tuple(offsets) if offsets is not None else uniform_offsets(num_chunks, chunk)
     return Workload(name, B, H, D, dtype, kind, offs, 0, tangent_std)

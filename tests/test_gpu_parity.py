@@ -247,3 +247,63 @@ def test_full_mask_growing_scores():
     errs = (_rel(_np(o), O), _rel(_np(do), dO), _rel(_np(lse), LSE))
     _say(f"[rescale] full rel-L2 O={errs[0]:.3e} dO={errs[1]:.3e} LSE={errs[2]:.3e}")
     assert max(errs) <= TOL["bf16"], errs
+
+
+# ----------------------------------------------------------------------------- explicit range lists
+
+def _random_ranges(L, G, seed):
+    rng = np.random.default_rng(seed)
+    cuts = np.sort(rng.choice(np.arange(1, L), size=G - 1, replace=False))
+    groups = []
+    for e in list(cuts) + [L]:
+        a0, a1, b0, b1 = (int(v) for v in np.sort(rng.integers(0, L + 1, size=4)))
+        if rng.random() < 0.15:
+            a1 = a0
+        if rng.random() < 0.3:
+            b1 = b0
+        groups.append((int(e), a0, a1, b0, b1))
+    return groups
+
+
+def _check_ranges(w, seed):
+    x = make_inputs(w, "cpu", seed)
+    o, do, lse = _run_gpu(w, x)
+    O, dO, LSE = attention_jvp(*[_np(x[k]) for k in ("Q", "K", "V", "dQ", "dK", "dV")], w.kind, _offsets(w))
+    lse_g = _np(lse)
+    dead = ~np.isfinite(LSE)
+    # rows with no admissible key: O = dO = 0 and LSE = -inf exactly
+    assert np.array_equal(np.isneginf(lse_g), dead)
+    assert np.all(_np(o)[np.broadcast_to(dead[..., None], O.shape)] == 0)
+    assert np.all(_np(do)[np.broadcast_to(dead[..., None], dO.shape)] == 0)
+    errs = (_rel(_np(o), O), _rel(_np(do), dO), _rel(lse_g[~dead], LSE[~dead]))
+    _say(f"[ranges] {w.name} dead rows={int(dead.sum())} rel-L2 O={errs[0]:.3e} dO={errs[1]:.3e} LSE={errs[2]:.3e}")
+    assert max(errs) <= TOL[w.dtype], errs
+
+
+@pytest.mark.parametrize("dt,D,L,G,seed", [("bf16", 128, 700, 9, 1), ("bf16", 128, 1500, 40, 2),
+                                           ("bf16", 64, 333, 5, 3), ("f32", 128, 200, 6, 4),
+                                           ("f32", 64, 97, 12, 5)])
+def test_random_range_lists(dt, D, L, G, seed):
+    groups = _random_ranges(L, G, seed)
+    if seed == 1:
+        groups[0] = (groups[0][0], 0, 0, 0, 0)  # guarantee a fully masked group
+    w = custom_workload(f"ranges_{dt}_{D}_{L}_{G}", 1, 2, D, dt, "ranges", offsets=groups, tangent_std=0.5)
+    _say(f"[ranges] {w.name} groups={groups[:3]}...")
+    _check_ranges(w, seed)
+
+
+def test_ranges_equal_to_tf_layout_match_tf_bitwise():
+    """The TF mask given as an explicit group table runs the same schedule, so the
+    outputs are bit-identical to the teacher-forcing layout."""
+    N, C = 3, 100
+    half = N * C
+    groups = [((j + 1) * C, 0, (j + 1) * C, 0, 0) for j in range(N)]
+    groups += [(half + (i + 1) * C, 0, i * C, half + i * C, half + (i + 1) * C) for i in range(N)]
+    w_tf = custom_workload("tf_as_tf", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, N, C, tangent_std=0.5)
+    w_rg = custom_workload("tf_as_ranges", 1, 2, 128, "bf16", "ranges", offsets=groups, tangent_std=0.5)
+    _say("[ranges] TF table vs TF layout")
+    x = make_inputs(w_tf, "cpu", 11)
+    a = _run_gpu(w_tf, x)
+    b = _run_gpu(w_rg, x)
+    for u, v in zip(a, b):
+        assert torch.equal(u, v)

@@ -10,7 +10,8 @@ import re
 import numpy as np
 import pytest
 
-from oracle import MASK_BLOCK_CAUSAL, MASK_FULL, MASK_TEACHER_FORCING, allowed_mask, count_allowed_pairs
+from oracle import (MASK_BLOCK_CAUSAL, MASK_FULL, MASK_RANGES, MASK_TEACHER_FORCING, allowed_mask,
+                    count_allowed_pairs)
 from paper_2606_25473_amd import binding
 from paper_2606_25473_amd.binding import make_layout
 from paper_2606_25473_amd.workloads import WORKLOADS
@@ -26,7 +27,26 @@ LAYOUTS = [
     (MASK_BLOCK_CAUSAL, [0, 50, 77, 200, 333], 333),
     (MASK_FULL, None, 1000),
     (MASK_FULL, None, 7),
+    (MASK_RANGES, [(100, 0, 0, 0, 0), (300, 0, 50, 250, 300), (301, 0, 301, 0, 0), (520, 400, 520, 10, 20)], 520),
+    (MASK_RANGES, [(7, 3, 5, 0, 0)], 7),
 ]
+
+
+def random_ranges(L, G, seed):
+    """Seeded random query groups with two non-overlapping key ranges (some empty)."""
+    rng = np.random.default_rng(seed)
+    cuts = np.sort(rng.choice(np.arange(1, L), size=G - 1, replace=False))
+    ends = list(cuts) + [L]
+    groups = []
+    for e in ends:
+        p = np.sort(rng.integers(0, L + 1, size=4))
+        a0, a1, b0, b1 = (int(v) for v in p)
+        if rng.random() < 0.15:
+            a1 = a0
+        if rng.random() < 0.3:
+            b1 = b0
+        groups.append((int(e), a0, a1, b0, b1))
+    return groups
 
 
 @pytest.fixture(scope="module")
@@ -76,6 +96,15 @@ def test_query_groups_reproduce_mask(lib, kind, offsets, L):
         m[q0:q1, b0:b1] = True
     assert prev == L
     assert np.array_equal(m, allowed_mask(kind, offsets, L))
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_range_lists(lib, seed):
+    L = int(np.random.default_rng(seed).integers(40, 900))
+    groups = random_ranges(L, 1 + seed * 7, seed)
+    assert binding.count_unmasked_pairs("ranges", groups, L) == count_allowed_pairs(MASK_RANGES, groups, L)
+    test_query_groups_reproduce_mask(lib, MASK_RANGES, groups, L)
+    test_tile_plans_cover_mask_and_full_blocks_are_full(lib, MASK_RANGES, groups, L)
 
 
 @pytest.mark.parametrize("kind,offsets,L", LAYOUTS)
@@ -153,6 +182,11 @@ def _call(lib, **kw):
     (dict(layout=make_layout("block_causal", [0, 10, 20]), L=64), 1, "block-causal"),
     (dict(layout=make_layout("teacher_forcing", list(range(66))), L=130), 1, "num_chunks"),
     (dict(layout=make_layout(9)), 1, "kind"),
+    (dict(layout=make_layout("ranges", [(30, 0, 10, 5, 20), (64, 0, 64, 0, 0)])), 1, "overlap"),
+    (dict(layout=make_layout("ranges", [(30, 0, 10, 0, 0), (60, 0, 64, 0, 0)])), 1, "cover"),
+    (dict(layout=make_layout("ranges", [(30, 0, 10, 0, 0), (30, 0, 64, 0, 0)])), 1, "increasing"),
+    (dict(layout=make_layout("ranges", [(64, 0, 65, 0, 0)])), 1, "begin <= end <= L"),
+    (dict(layout=make_layout("ranges", [])), 1, "query groups"),
 ])
 @_no_gpu
 def test_invalid_arguments_are_rejected_before_any_hip_call(lib, kw, code, needle):

@@ -17,7 +17,7 @@ import torch
 import torch.nn.functional as F
 from torch.nn.attention import SDPBackend, sdpa_kernel
 
-from oracle import (MASK_BLOCK_CAUSAL, MASK_FULL, MASK_TEACHER_FORCING, allowed_mask,
+from oracle import (MASK_BLOCK_CAUSAL, MASK_FULL, MASK_RANGES, MASK_TEACHER_FORCING, allowed_mask,
                     attention_fwd, attention_jvp, count_allowed_pairs)
 from oracle.dual import attention_dual
 
@@ -67,6 +67,28 @@ def test_nonuniform_tf_mask_matches_hand_written():
     m, offsets = _read_mask("tf_mask_nonuniform.txt")
     assert offsets == [0, 1, 3]
     assert np.array_equal(allowed_mask(MASK_TEACHER_FORCING, offsets, 6), m)
+
+
+def test_ranges_mask_reproduces_hand_written_tf_mask():
+    # the TF mask of the golden fixture, given as query groups with key ranges
+    m, _ = _read_mask("tf_mask_N3_C2.txt")
+    groups = [(2, 0, 2, 0, 0), (4, 0, 4, 0, 0), (6, 0, 6, 0, 0),
+              (8, 0, 0, 6, 8), (10, 0, 2, 8, 10), (12, 0, 4, 10, 12)]
+    assert np.array_equal(allowed_mask(MASK_RANGES, groups, 12), m)
+
+
+def test_ranges_mask_with_empty_group_and_two_ranges():
+    groups = [(1, 0, 0, 0, 0), (3, 1, 2, 4, 5), (5, 0, 5, 0, 0)]
+    want = np.array([[0, 0, 0, 0, 0], [0, 1, 0, 0, 1], [0, 1, 0, 0, 1], [1, 1, 1, 1, 1], [1, 1, 1, 1, 1]], bool)
+    assert np.array_equal(allowed_mask(MASK_RANGES, groups, 5), want)
+
+
+def test_fully_masked_rows_give_zero_and_minus_inf():
+    groups = [(2, 0, 0, 0, 0), (5, 0, 5, 0, 0)]
+    x = [_rand((1, 1, 5, 4), 200 + s) for s in range(6)]
+    O, dO, LSE = attention_jvp(*x, MASK_RANGES, groups)
+    assert np.all(O[0, 0, :2] == 0) and np.all(dO[0, 0, :2] == 0) and np.all(LSE[0, 0, :2] == -np.inf)
+    assert np.all(np.isfinite(O[0, 0, 2:])) and np.all(np.isfinite(LSE[0, 0, 2:]))
 
 
 @pytest.mark.parametrize("N,C", [(1, 1), (3, 5), (4, 16), (7, 13), (21, 3)])
