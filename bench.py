@@ -1,11 +1,17 @@
 """Throughput of the fused masked attention forward + JVP on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--forward] [--no-cpu]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--forward | --zero-clean]
+                    [--no-cpu]
 
 One step = one ``attn_jvp_fwd`` call over the whole batch of the workload
 (default: Wan2.1-1.3B chunk-wise teacher forcing, B=1, H=12, L=65520, D=128,
 bf16), inputs already resident in HBM.  Work is counted over admissible
 (query, key) pairs only: 12*D flop per pair for the JVP, 4*D for the forward.
+``--zero-clean`` times ``attn_jvp_fwd_zero_clean`` instead (teacher-forcing
+workloads: tangents of the noisy half only) and counts the work that variant
+must do: 4*D per pair of a clean query, 8*D per (noisy query, clean key) pair
+(scores, dQ term, output, H~ term), 12*D per (noisy query, noisy key) pair; it
+also reports the dense JVP's time on the same inputs.
 Prints ONE JSON line.  The ``cpu_baseline`` leg times the fp64 CPU oracle on a
 bounded sample of query rows of the same workload (and checks the sampled GPU
 rows against it).
@@ -23,7 +29,8 @@ import torch
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from paper_2606_25473_amd import attn_fwd, attn_jvp_fwd, count_computed_pairs, count_unmasked_pairs  # noqa: E402
+from paper_2606_25473_amd import (attn_fwd, attn_jvp_fwd, attn_jvp_fwd_zero_clean, count_computed_pairs,  # noqa: E402
+                                  count_unmasked_pairs, query_groups)
 from paper_2606_25473_amd.workloads import HEADLINE, WORKLOADS, make_inputs  # noqa: E402
 
 METRIC = "masked attention fwd+JVP TFLOP/s (unmasked pairs) and % bf16 MFMA peak"
@@ -42,7 +49,26 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def profile_record(workload, forward):
+def zero_clean_flop(groups, half, D):
+    """Flop per (batch, head) of the zero-clean JVP from the query-group table
+    [(q0, q1, a0, a1, b0, b1)]: 4D per pair of a clean query, 8D per (noisy query,
+    clean key) pair, 12D per (noisy query, noisy key) pair."""
+    total = 0
+    for q0, q1, a0, a1, b0, b1 in groups:
+        for r0, r1 in ((q0, min(q1, half)), (max(q0, half), q1)):
+            if r1 <= r0:
+                continue
+            for k0, k1 in ((a0, a1), (b0, b1)):
+                clean_keys = max(0, min(k1, half) - k0)
+                noisy_keys = max(0, k1 - max(k0, half))
+                if r1 <= half:
+                    total += (r1 - r0) * (clean_keys + noisy_keys) * 4 * D
+                else:
+                    total += (r1 - r0) * (clean_keys * 8 + noisy_keys * 12) * D
+    return total
+
+
+def profile_record(workload, mode):
     """The committed rocprofv3 counter record of this workload (HBM bytes per launch,
     shader clock, MFMA busy fraction), if it was taken on the current kernel source;
     else an empty dict."""
@@ -51,15 +77,16 @@ def profile_record(workload, forward):
         return {}
     with open(path) as f:
         rec = json.load(f)
-    ent = rec.get(f"{workload}:{'fwd' if forward else 'jvp'}")
+    ent = rec.get(f"{workload}:{mode}")
     if not ent or ent.get("kernel_source_hash") != kernel_source_hash():
         return {}
     return ent
 
 
-def cpu_baseline(w, x, out, forward, budget_s=15.0):
+def cpu_baseline(w, x, out, mode, budget_s=15.0):
     """Time the fp64 CPU oracle on a bounded sample of rows of head (0, 0)."""
-    from oracle import allowed_mask, attention_fwd, attention_jvp  # the oracle is only used on this leg
+    # the oracle is only used on this leg
+    from oracle import allowed_mask, attention_fwd, attention_jvp, attention_jvp_zero_clean
     try:
         from threadpoolctl import threadpool_info
         blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
@@ -67,34 +94,51 @@ def cpu_baseline(w, x, out, forward, budget_s=15.0):
         blas_name = blas[0].get("internal_api", "?") if blas else "?"
     except Exception:  # threadpoolctl missing
         cores, blas_name = os.cpu_count(), "?"
-    L = w.L
+    L, D = w.L, w.D
+    half = L // 2
     h = {k: v[0:1, 0:1].float().cpu().numpy() for k, v in x.items()}
     offs = list(w.offsets) or None
     # rows spread evenly over the sequence so the per-row key-count mix matches the workload
     order = np.random.default_rng(0).permutation(L)
-    done, t_used, pairs, flop_per_pair = 0, 0.0, 0, (4 if forward else 12) * w.D
+    done, t_used, pairs, flop = 0, 0.0, 0, 0
     errs = []
-    got_o, got_do = out[0][0, 0], (None if forward else out[1][0, 0])
+    got_o, got_do = out[0][0, 0], (None if mode == "fwd" else out[1][0, 0])
     batch = 256
     while t_used < budget_s and done < L:
         rows = np.sort(order[done:done + batch])
         t0 = time.perf_counter()
-        if forward:
+        if mode == "fwd":
             O, _ = attention_fwd(h["Q"], h["K"], h["V"], w.kind, offs, rows=rows)
             dO = None
+        elif mode == "zc":
+            O, dO, _ = attention_jvp_zero_clean(h["Q"], h["K"], h["V"], h["dQn"], h["dKn"], h["dVn"], offs,
+                                                rows=rows)
         else:
             O, dO, _ = attention_jvp(h["Q"], h["K"], h["V"], h["dQ"], h["dK"], h["dV"], w.kind, offs, rows=rows)
         t_used += time.perf_counter() - t0
         done += len(rows)
-        pairs += int(allowed_mask(w.kind, offs, L, rows).sum())
+        m = allowed_mask(w.kind, offs, L, rows)
+        pairs += int(m.sum())
+        if mode == "zc":
+            clean_q = rows < half
+            ck, nk = m[:, :half].sum(1), m[:, half:].sum(1)
+            flop += int((4 * (ck + nk))[clean_q].sum() + (8 * ck + 12 * nk)[~clean_q].sum()) * D
+        else:
+            flop += int(m.sum()) * (4 if mode == "fwd" else 12) * D
         r = torch.from_numpy(rows).to(got_o.device)
         g = got_o.index_select(0, r).float().cpu().numpy()
         errs.append((np.linalg.norm(g - O[0, 0]) ** 2, np.linalg.norm(O[0, 0]) ** 2))
         if dO is not None:
-            gd = got_do.index_select(0, r).float().cpu().numpy()
+            if mode == "zc":   # the GPU's dO holds the noisy rows only; the clean rows' is zero
+                sel = rows >= half
+                gd = np.zeros_like(dO[0, 0])
+                gd[sel] = got_do.index_select(0, torch.from_numpy(rows[sel] - half).to(got_do.device)) \
+                    .float().cpu().numpy()
+            else:
+                gd = got_do.index_select(0, r).float().cpu().numpy()
             errs.append((np.linalg.norm(gd - dO[0, 0]) ** 2, np.linalg.norm(dO[0, 0]) ** 2))
     rel = float(np.sqrt(sum(e for e, _ in errs) / max(sum(n for _, n in errs), 1e-300)))
-    value = pairs * flop_per_pair / t_used / 1e12
+    value = flop / t_used / 1e12
     return {"value": value, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
             "sample": f"{done} query rows of head (0,0) spread over the {L}-token sequence "
                       f"({pairs} admissible pairs, {t_used:.1f} s, fp64 numpy/{blas_name})",
@@ -108,6 +152,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=HEADLINE, choices=sorted(WORKLOADS))
     ap.add_argument("--forward", action="store_true", help="time attn_fwd instead of attn_jvp_fwd")
+    ap.add_argument("--zero-clean", action="store_true",
+                    help="time attn_jvp_fwd_zero_clean (teacher forcing, zero clean-half tangents)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -122,6 +168,11 @@ def main():
         sys.exit(1)
 
     w = WORKLOADS[args.workload]
+    if args.forward and args.zero_clean:
+        ap.error("--forward and --zero-clean are exclusive")
+    if args.zero_clean and w.kind != "teacher_forcing":
+        ap.error("--zero-clean needs a teacher-forcing workload")
+    mode = "fwd" if args.forward else ("zc" if args.zero_clean else "jvp")
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     x = make_inputs(w, "cuda", seed=0)
@@ -131,10 +182,19 @@ def main():
     o = torch.empty_like(q)
     do = torch.empty_like(q)
     lse = torch.empty((B, H, L), device=dev, dtype=torch.float32)
+    half = L // 2
+    if mode == "zc":  # tangents of the noisy half only
+        for n in ("dQ", "dK", "dV"):
+            x[n + "n"] = x.pop(n)[:, :, half:].contiguous()
+        dqn, dkn, dvn = x["dQn"], x["dKn"], x["dVn"]
+        del dq, dk, dv
+        don = torch.empty_like(dqn)
 
     def step():
-        if args.forward:
+        if mode == "fwd":
             attn_fwd(q, k, v, w.kind, offs, out=(o, lse))
+        elif mode == "zc":
+            attn_jvp_fwd_zero_clean(q, k, v, dqn, dkn, dvn, offs, out=(o, don, lse))
         else:
             attn_jvp_fwd(q, k, v, dq, dk, dv, w.kind, offs, out=(o, do, lse))
 
@@ -165,12 +225,14 @@ def main():
 
     pairs = count_unmasked_pairs(w.kind, offs, L)
     computed = count_computed_pairs(w.kind, offs, L, D)
-    flop_per_pair = (4 if args.forward else 12) * D
-    flop = pairs * flop_per_pair * B * H
+    if mode == "zc":
+        flop = zero_clean_flop(query_groups(w.kind, offs, L), half, D) * B * H
+    else:
+        flop = pairs * (4 if mode == "fwd" else 12) * D * B * H
     value = flop / (ms_per_step * 1e-3) / 1e12
     achieved = flop / (kernel_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_TFLOPS
-    prof = profile_record(w.name, args.forward)
+    prof = profile_record(w.name, mode)
     traffic = prof.get("hbm_bytes_per_launch")
     res = {
         "metric": METRIC,
@@ -185,7 +247,7 @@ def main():
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic",
-        "config": dict(w.describe(), op="attn_fwd" if args.forward else "attn_jvp_fwd"),
+        "config": dict(w.describe(), op={"fwd": "attn_fwd", "zc": "attn_jvp_fwd_zero_clean"}.get(mode, "attn_jvp_fwd")),
         "pct_peak": round(100 * achieved / peak, 2),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": round(peak, 1),
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
@@ -201,8 +263,27 @@ def main():
         res["roofline"]["measured_clock_ghz"] = round(clk, 3)
         res["roofline"]["frac_at_measured_clock"] = round(achieved / (peak * clk / 2.4), 4)
         res["roofline"]["mfma_busy_cycles_frac"] = round(prof.get("mfma_busy", 0.0), 4)
+    if mode == "zc":
+        # the dense JVP of the same function (tangents zero-padded over the clean half)
+        pad = {n: torch.cat([torch.zeros_like(x[n + "n"]), x[n + "n"]], dim=2) for n in ("dQ", "dK", "dV")}
+        o2, do2 = torch.empty_like(q), torch.empty_like(q)
+        for _ in range(args.warmup):
+            attn_jvp_fwd(q, k, v, pad["dQ"], pad["dK"], pad["dV"], w.kind, offs, out=(o2, do2, lse))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            attn_jvp_fwd(q, k, v, pad["dQ"], pad["dK"], pad["dV"], w.kind, offs, out=(o2, do2, lse))
+        e1.record(stream)
+        torch.cuda.synchronize()
+        dense_ms = e0.elapsed_time(e1) / args.steps
+        res["dense_jvp_kernel_ms"] = round(dense_ms, 4)
+        res["speedup_vs_dense_jvp"] = round(dense_ms / kernel_ms, 3)
+        res["zero_clean_flop_over_dense"] = round(flop / (pairs * 12 * D * B * H), 4)
+        del pad, o2, do2
+        step()  # restore the outputs the CPU leg compares against
+        torch.cuda.synchronize()
     if not args.no_cpu:
-        res["cpu_baseline"] = cpu_baseline(w, x, (o, do, lse), args.forward, args.cpu_budget)
+        res["cpu_baseline"] = cpu_baseline(w, x, (o, don if mode == "zc" else do, lse), mode, args.cpu_budget)
     print(json.dumps(res), flush=True)
 
 

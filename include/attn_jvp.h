@@ -104,6 +104,30 @@ int attn_jvp_fwd(int dtype, int B, int H, int L, int D,
                  const attn_chunk_layout* layout, float softmax_scale,
                  void* O, void* dO, float* LSE, void* stream);
 
+/* Fused forward + JVP for the teacher-forcing sCM tangent (paper Sec. 3.1.2, the
+ * TF-sCM tangent equation: the packed input tangent is [0^clean, t^noisy], i.e. the
+ * clean context carries zero tangent).  `layout` must be ATTN_MASK_TEACHER_FORCING;
+ * with half = L / 2 the tangents of the clean rows [0, half) are zero and are not
+ * passed:
+ *   in : Q, K, V              device [B, H, L, D]
+ *        dQn, dKn, dVn        device [B, H, L - half, D]: tangents of the noisy rows
+ *                             [half, L) (row x of the sequence is row x - half here)
+ *   out: O                    device [B, H, L, D]
+ *        dOn                  device [B, H, L - half, D]: dO of the noisy rows
+ *        LSE                  device fp32 [B, H, L]
+ * The result equals attn_jvp_fwd on the zero-padded tangents [0, dQn] etc.; the dO
+ * of the clean rows is exactly zero (a clean query sees clean keys only, whose K and
+ * V tangents vanish, and its own dQ vanishes), so it is not written.  The kernels
+ * skip the work the zeros make vanish: clean query tiles run the forward only, and
+ * noisy queries drop the dK and dV terms over clean keys.  Same conventions, dtypes
+ * and error behaviour as attn_jvp_fwd; a layout of another kind is
+ * ATTN_ERR_INVALID. */
+int attn_jvp_fwd_zero_clean(int dtype, int B, int H, int L, int D,
+                            const void* Q, const void* K, const void* V,
+                            const void* dQn, const void* dKn, const void* dVn,
+                            const attn_chunk_layout* layout, float softmax_scale,
+                            void* O, void* dOn, float* LSE, void* stream);
+
 /* Masked attention forward only (the primal part of Algorithm 1): O and LSE
  * exactly as attn_jvp_fwd would produce them from the same Q, K, V. */
 int attn_fwd(int dtype, int B, int H, int L, int D,
@@ -142,6 +166,14 @@ void attn_tile_shape(int* rows_per_tile, int* keys_per_block);
  * or a too-small buffer (capacity `cap`). */
 int attn_tile_plan(const attn_chunk_layout* layout, int L, int qtile,
                    int32_t* blocks, int32_t* full, int cap);
+
+/* Host only.  Order in which the bf16 kernels' work-groups of one (batch, head)
+ * take query tiles: order[t] = query tile of the t-th work-group (a permutation
+ * of 0 .. ceil(L / R) - 1, heaviest tiles first where the layout makes the
+ * per-tile work predictable).  zero_clean != 0 gives the order of
+ * attn_jvp_fwd_zero_clean, else that of attn_jvp_fwd / attn_fwd.  Returns the
+ * number of tiles, or -1 on an invalid layout or a too-small buffer. */
+int attn_tile_order(const attn_chunk_layout* layout, int L, int zero_clean, int32_t* order, int cap);
 
 /* Thread-local description of the last nonzero return on this thread ("" if none). */
 const char* attn_last_error(void);

@@ -11,7 +11,9 @@ masks      -- the attention mask materialised from its definition (per-token
               chunk ids), for the full, block-causal and teacher-forcing kinds,
               and from an explicit query-group / key-range list.
 attention  -- closed-form masked attention O, LSE and the forward-mode tangent
-              dO (paper, App. B, the masked-attention and tangent equations).
+              dO (paper, App. B, the masked-attention and tangent equations),
+              and the same JVP with zero tangents on the clean half of a
+              teacher-forcing sequence (paper Sec. 3.1.2, TF-sCM tangent).
 dual       -- a pure-Python dual-number evaluation of the same map, used on
               tiny inputs to pin the closed form (no closed-form tangent used).
 
@@ -21,9 +23,9 @@ scaled_dot_product_attention and torch.func.jvp, the two-pass TF identity,
 hand-derived golden values and invariants).
 """
 from .masks import MASK_FULL, MASK_BLOCK_CAUSAL, MASK_TEACHER_FORCING, MASK_RANGES, allowed_mask, count_allowed_pairs
-from .attention import attention_jvp, attention_fwd
+from .attention import attention_jvp, attention_fwd, attention_jvp_zero_clean
 
 __all__ = [
     "MASK_FULL", "MASK_BLOCK_CAUSAL", "MASK_TEACHER_FORCING", "MASK_RANGES",
-    "allowed_mask", "count_allowed_pairs", "attention_jvp", "attention_fwd",
+    "allowed_mask", "count_allowed_pairs", "attention_jvp", "attention_fwd", "attention_jvp_zero_clean",
 ]

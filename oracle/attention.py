@@ -24,7 +24,7 @@ of the blocking.
 """
 import numpy as np
 
-from .masks import allowed_mask
+from .masks import MASK_TEACHER_FORCING, allowed_mask
 
 
 def _f64(x):
@@ -102,3 +102,21 @@ def attention_fwd(Q, K, V, kind, offsets=None, scale=None, rows=None, block=256)
     """(O, LSE) in fp64: the primal part of :func:`attention_jvp`."""
     O, _, LSE = _run(Q, K, V, None, None, None, kind, offsets, scale, rows, block, False)
     return O, LSE
+
+
+def attention_jvp_zero_clean(Q, K, V, dQn, dKn, dVn, offsets, scale=None, rows=None, block=256):
+    """(O, dO, LSE) in fp64 of teacher-forcing attention whose clean half has zero tangent.
+
+    Paper Sec. 3.1.2, the TF-sCM tangent equation: the JVP runs through the packed
+    [clean | noisy] forward with input tangent [0^clean, t^noisy].  Q, K, V are
+    [B, H, L, D] over the packed sequence; dQn, dKn, dVn are [B, H, L - L/2, D], the
+    tangents of the noisy rows.  This is the definition written out: the tangents
+    are padded with zeros over the clean rows and :func:`attention_jvp` is taken
+    with the teacher-forcing mask.  dO is returned for every row (``rows`` selects
+    sequence rows, as in :func:`attention_jvp`); its clean rows come out zero.
+    """
+    Q = _f64(Q)
+    half = Q.shape[2] // 2
+    pad = lambda t: np.concatenate([np.zeros(Q.shape[:2] + (half, Q.shape[3])), _f64(t)], axis=2)
+    return attention_jvp(Q, K, V, pad(dQn), pad(dKn), pad(dVn), MASK_TEACHER_FORCING, offsets, scale,
+                         rows, block)

@@ -52,6 +52,8 @@ def load_library():
     lib.attn_jvp_fwd.argtypes = [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp,
                                  ctypes.POINTER(_Layout), ctypes.c_float, _vp, _vp, _vp, _vp]
     lib.attn_jvp_fwd.restype = _i
+    lib.attn_jvp_fwd_zero_clean.argtypes = lib.attn_jvp_fwd.argtypes
+    lib.attn_jvp_fwd_zero_clean.restype = _i
     lib.attn_fwd.argtypes = [_i, _i, _i, _i, _i, _vp, _vp, _vp,
                              ctypes.POINTER(_Layout), ctypes.c_float, _vp, _vp, _vp]
     lib.attn_fwd.restype = _i
@@ -66,6 +68,8 @@ def load_library():
     lib.attn_tile_plan.argtypes = [ctypes.POINTER(_Layout), _i, _i, ctypes.POINTER(ctypes.c_int32),
                                    ctypes.POINTER(ctypes.c_int32), _i]
     lib.attn_tile_plan.restype = _i
+    lib.attn_tile_order.argtypes = [ctypes.POINTER(_Layout), _i, _i, ctypes.POINTER(ctypes.c_int32), _i]
+    lib.attn_tile_order.restype = _i
     lib.attn_last_error.argtypes = []
     lib.attn_last_error.restype = ctypes.c_char_p
     _lib = lib
@@ -108,14 +112,16 @@ def _dtype_code(t):
     raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
 
 
-def _check_inputs(ts):
+def _check_inputs(ts, shape=None):
+    """All of ``ts`` on q's device with q's dtype, contiguous, of ``shape`` (q's by default)."""
     q = ts[0]
     if q.dim() != 4:
         raise ValueError("tensors must be [B, H, L, D]")
+    shape = q.shape if shape is None else shape
     for t in ts:
         if not t.is_cuda:
             raise ValueError("tensors must live on a GPU")
-        if t.device != q.device or t.dtype != q.dtype or t.shape != q.shape:
+        if t.device != q.device or t.dtype != q.dtype or t.shape != shape:
             raise ValueError("all inputs need the same device, dtype and shape")
         if not t.is_contiguous():
             raise ValueError("inputs must be contiguous")
@@ -146,6 +152,38 @@ def attn_jvp_fwd(q, k, v, dq, dk, dv, kind="teacher_forcing", offsets=None, scal
                               st.cuda_stream)
     _check(rc)
     return o, do, lse
+
+
+def attn_jvp_fwd_zero_clean(q, k, v, dqn, dkn, dvn, offsets, scale=None, out=None, stream=None):
+    """(O, dOn, LSE) of teacher-forcing attention whose clean half has zero tangent.
+
+    q, k, v: contiguous [B, H, L, D] GPU tensors over the packed [clean | noisy]
+    sequence; dqn, dkn, dvn: [B, H, L/2, D] tangents of the noisy half only.
+    Returns O [B, H, L, D], dOn [B, H, L/2, D] (dO of the noisy half; the clean
+    half's is zero) and LSE [B, H, L].  ``offsets``: chunk prefix offsets.
+    """
+    lib = load_library()
+    _check_inputs([q, k, v])
+    B, H, L, D = q.shape
+    nshape = torch.Size((B, H, L - L // 2, D))
+    _check_inputs([dqn, dkn, dvn], nshape)
+    if dqn.device != q.device or dqn.dtype != q.dtype:
+        raise ValueError("tangents need q's device and dtype")
+    if out is None:
+        o = torch.empty_like(q)
+        don = torch.empty(nshape, device=q.device, dtype=q.dtype)
+        lse = torch.empty((B, H, L), device=q.device, dtype=torch.float32)
+    else:
+        o, don, lse = out
+    lay = make_layout("teacher_forcing", offsets)
+    st = stream if stream is not None else torch.cuda.current_stream(q.device)
+    with torch.cuda.device(q.device):
+        rc = lib.attn_jvp_fwd_zero_clean(_dtype_code(q), B, H, L, D, q.data_ptr(), k.data_ptr(),
+                                         v.data_ptr(), dqn.data_ptr(), dkn.data_ptr(), dvn.data_ptr(),
+                                         ctypes.byref(lay), float(scale or 0.0), o.data_ptr(),
+                                         don.data_ptr(), lse.data_ptr(), st.cuda_stream)
+    _check(rc)
+    return o, don, lse
 
 
 def attn_fwd(q, k, v, kind="teacher_forcing", offsets=None, scale=None, out=None, stream=None):
@@ -199,6 +237,18 @@ def tile_shape():
     r, k = _i(), _i()
     load_library().attn_tile_shape(ctypes.byref(r), ctypes.byref(k))
     return r.value, k.value
+
+
+def tile_order(kind, offsets, L, zero_clean=False):
+    """Query tile taken by the t-th work-group of a (batch, head), for t = 0, 1, ..."""
+    R, _ = tile_shape()
+    cap = (int(L) + R - 1) // R
+    buf = (ctypes.c_int32 * max(cap, 1))()
+    n = load_library().attn_tile_order(ctypes.byref(make_layout(kind, offsets)), int(L),
+                                       1 if zero_clean else 0, buf, cap)
+    if n < 0:
+        raise AttnError(1, last_error())
+    return list(buf[:n])
 
 
 def tile_plan(kind, offsets, L, qtile):

@@ -122,43 +122,67 @@ __device__ __forceinline__ unsigned lds_addr(const void* p) {
   return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
-template <int D, bool JVP>
-__global__ __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void attn_mfma_kernel(const AttnArgs a) {
+// Kernel variants.  kZeroClean is the JVP of a sequence whose rows below t0 carry
+// zero tangents (the clean context of the teacher-forcing sCM objective, paper
+// Sec. 3.1.2, packed input tangent [0^clean, t^noisy]).  Those rows and keys then
+// contribute nothing to dS or dO, so
+//  - a query tile wholly below t0 runs the forward body (its dO is zero);
+//  - a key block wholly below t0 drops dK Q^T and dV^T P~^T (dK = dV = 0 there);
+//  - the tangent tensors (and dO) hold the rows [t0, L) only.
+// A key block or query tile that straddles t0 runs the full JVP step with the
+// tangent rows below t0 cleared in LDS, so that every result equals the dense JVP
+// of the zero-padded tangents.
+enum { kFwd = 0, kJvp = 1, kZeroClean = 2 };
+
+template <bool B>
+struct Tag {
+  static constexpr bool value = B;
+};
+
+// One work-group's query tile `qtile` of (batch, head) `bh`.  `stages` and `sdQ`
+// are the work-group's LDS buffers (sized for the JVP bodies).
+template <int D, int MODE>
+__device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const int qtile,
+                                          char* const stages, char* const sdQ) {
+  constexpr bool JVP = MODE != kFwd;
+  constexpr bool ZC = MODE == kZeroClean;
   using G = Geo<D>;
   constexpr int TB = G::TILEB;
-  constexpr int TBJ = JVP ? G::TILEB : 16;      // tangent tiles exist only in the JVP kernel
-  constexpr int QB = JVP ? BR * G::ROWB : 16;   // dQ tile (JVP only)
+  constexpr int TBJ = JVP ? G::TILEB : 16;      // tangent tiles exist only in the JVP bodies
   // Three pipeline stages (block k is read from stage k mod 3 while block k+2 streams
   // into stage (k+2) mod 3), each holding the K, V, dK, dV tiles of one key block.
-  // dQ of the query tile lives in LDS too (read back as an MFMA operand), which keeps
-  // the per-wave register footprint within two waves per SIMD.
-  // D = 128 JVP: 3 x 32 KiB + 64 KiB = 160 KiB.
   constexpr int SB = 2 * TB + 2 * TBJ;
-  __shared__ __attribute__((aligned(1024))) char stages[3 * SB];
-  __shared__ __attribute__((aligned(1024))) char sdQ[QB];
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int lane = tid & 63;
   const int hh = lane >> 5;   // which half of the wave (key sub-block within S^T)
   const int L = a.L;
+  // tangent rows are [t0, L): t0 = 0 for the dense JVP
+  const int t0 = ZC ? a.t0 : 0;
+  const int Lt = L - t0;
 
-  const int nqt = a.order.nt;
-  const int bh = blockIdx.x / nqt;
-  const int qtile = tile_of(a.order, blockIdx.x - bh * nqt);
   const size_t head = (size_t)bh * L * D;
+  const size_t thead = (size_t)bh * Lt * D;
   const bf16_t* __restrict__ Qg = (const bf16_t*)a.Q + head;
   const bf16_t* __restrict__ Kg = (const bf16_t*)a.K + head;
   const bf16_t* __restrict__ Vg = (const bf16_t*)a.V + head;
-  const bf16_t* __restrict__ dQg = (const bf16_t*)a.dQ + head;
-  const bf16_t* __restrict__ dKg = (const bf16_t*)a.dK + head;
-  const bf16_t* __restrict__ dVg = (const bf16_t*)a.dV + head;
+  const bf16_t* __restrict__ dQg = (const bf16_t*)a.dQ + thead;
+  const bf16_t* __restrict__ dKg = (const bf16_t*)a.dK + thead;
+  const bf16_t* __restrict__ dVg = (const bf16_t*)a.dV + thead;
 
   const int q0 = qtile * BR;
   const int q1 = q0 + BR < L ? q0 + BR : L;
   const TilePlan plan = plan_tile(a.gt, q0, q1, BC);
   const int nblk = plan_num_blocks(plan);
+  // (kZeroClean) the plan visits key blocks in increasing key order: the first ntk of
+  // them hold no key >= t0
+  int ntk = 0;
+  if constexpr (ZC) {
+    const int kc = t0 / BC;
+    ntk = imin(imax(kc - plan.blk_begin0, 0), plan.blk_end0 - plan.blk_begin0) +
+          imin(imax(kc - plan.blk_begin1, 0), plan.blk_end1 - plan.blk_begin1);
+  }
 
   // ---- this lane's query row and its admissible key ranges
   const int qrow = wave * 32 + (lane & 31);   // row within the tile
@@ -194,6 +218,18 @@ void attn_mfma_kernel(const AttnArgs a) {
     const unsigned off = (grow * D + (unsigned)((dma_phys ^ swz<D>(rr)) * 8)) * 2u;
     lds_load16(src, off, dst + (unsigned)(r * G::ROWB));
   };
+  // tangent rows: sequence row x is tangent row x - t0; rows below t0 are clamped to
+  // tangent row 0 (finite data, cleared in LDS before use)
+  auto dma_rows_t = [&](const bf16_t* src, int row0, int r, unsigned dst) {
+    if constexpr (!ZC) {
+      dma_rows(src, row0, r, dst);
+    } else {
+      const int rr = r + dma_r;
+      const unsigned grow = (unsigned)min(max(row0 + rr - t0, 0), Lt - 1);
+      const unsigned off = (grow * D + (unsigned)((dma_phys ^ swz<D>(rr)) * 8)) * 2u;
+      lds_load16(src, off, dst + (unsigned)(r * G::ROWB));
+    }
+  };
   // one key tile of BC rows: instruction j (rows j*RPI ...) is issued by wave j % NW
   auto dma_tile = [&](const bf16_t* src, int k0, unsigned dst) {
 #pragma unroll
@@ -202,15 +238,30 @@ void attn_mfma_kernel(const AttnArgs a) {
       if (G::IPT % NW == 0 || j < G::IPT) dma_rows(src, k0, j * RPI, dst);
     }
   };
-  // the K, V, dK, dV tiles of key block kb into the stage at LDS address st
+  auto dma_tile_t = [&](const bf16_t* src, int k0, unsigned dst) {
+#pragma unroll
+    for (int j0 = 0; j0 < G::IPT; j0 += NW) {
+      const int j = j0 + wave;
+      if (G::IPT % NW == 0 || j < G::IPT) dma_rows_t(src, k0, j * RPI, dst);
+    }
+  };
+  // the K, V (and dK, dV) tiles of key block kb into the stage at LDS address st.  The
+  // tangent tiles are streamed for every block, also for blocks below t0 whose step does
+  // not read them (they then hold tangent row 0): a block-dependent load count would
+  // split the step into more basic blocks and cost registers the kernel does not have.
   auto dma_block = [&](int kb, unsigned st) {
     const int k0 = kb * BC;
     dma_tile(Kg, k0, st);
     dma_tile(Vg, k0, st + TB);
     if constexpr (JVP) {
-      dma_tile(dKg, k0, st + 2 * TB);
-      dma_tile(dVg, k0, st + 2 * TB + TBJ);
+      dma_tile_t(dKg, k0, st + 2 * TB);
+      dma_tile_t(dVg, k0, st + 2 * TB + TBJ);
     }
+  };
+  // clear the first nrows rows of an LDS tile (16 bytes per thread and pass)
+  auto zero_rows = [&](char* base, int nrows) {
+    const int n = nrows * (G::ROWB / 16);
+    for (int c = tid; c < n; c += NTHREADS) *(u32x4*)(base + 16 * c) = u32x4{0u, 0u, 0u, 0u};
   };
 
   // per-lane LDS offsets of the transposed V / dV operand reads:
@@ -254,11 +305,12 @@ void attn_mfma_kernel(const AttnArgs a) {
     else asm volatile("s_waitcnt vmcnt(2) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   };
 
-  // One key block.  Returns true -- before touching any accumulator -- if some row's
-  // block max exceeds its reference by more than kLazy; the caller then rescales and
-  // redoes the block.
-  auto step = [&](int it, const char* cK, const char* cV, const char* cdK, const char* cdV,
+  // One key block; TK: the block has tangent keys (dK, dV tiles are present).  Returns
+  // true -- before touching any accumulator -- if some row's block max exceeds its
+  // reference by more than kLazy; the caller then rescales and redoes the block.
+  auto step = [&](auto tk, int it, const char* cK, const char* cV, const char* cdK, const char* cdV,
                   unsigned next_stage) -> bool {
+    constexpr bool TK = JVP && decltype(tk)::value;
     // prefetch block it+2 into the stage freed by block it-1: a fixed number of loads
     // per iteration (indices past the end are clamped; that stage is never read)
     dma_block(plan_block(plan, min(it + 2, nblk - 1)), next_stage);
@@ -272,9 +324,11 @@ void attn_mfma_kernel(const AttnArgs a) {
       const bf16x8 kop = *(const bf16x8*)(cK + off);
       S = mfma(kop, qop[s], S);
       if constexpr (JVP) {
-        const bf16x8 dkop = *(const bf16x8*)(cdK + off);
         const bf16x8 dqop = *(const bf16x8*)(sdQ + lds_off<D>(qrow, 2 * s + hh));
-        dS = mfma(dkop, qop[s], dS);
+        if constexpr (TK) {
+          const bf16x8 dkop = *(const bf16x8*)(cdK + off);
+          dS = mfma(dkop, qop[s], dS);
+        }
         dS = mfma(kop, dqop, dS);
       }
     }
@@ -336,8 +390,10 @@ void attn_mfma_kernel(const AttnArgs a) {
         const bf16x8 vop = cat(ld_tr(cV + tro[t][0][dt]), ld_tr(cV + tro[t][1][dt]));
         oacc[dt] = mfma(vop, pb, oacc[dt]);
         if constexpr (JVP) {
-          const bf16x8 dvop = cat(ld_tr(cdV + tro[t][0][dt]), ld_tr(cdV + tro[t][1][dt]));
-          tacc[dt] = mfma(dvop, pb, tacc[dt]);
+          if constexpr (TK) {
+            const bf16x8 dvop = cat(ld_tr(cdV + tro[t][0][dt]), ld_tr(cdV + tro[t][1][dt]));
+            tacc[dt] = mfma(dvop, pb, tacc[dt]);
+          }
           tacc[dt] = mfma(vop, hb, tacc[dt]);
         }
       }
@@ -352,7 +408,7 @@ void attn_mfma_kernel(const AttnArgs a) {
   if constexpr (JVP) {
     const unsigned dq_lds = __builtin_amdgcn_readfirstlane(lds_addr(sdQ));
 #pragma unroll
-    for (int j0 = 0; j0 < G::IPQ; j0 += NW) dma_rows(dQg, q0, (j0 + wave) * RPI, dq_lds);
+    for (int j0 = 0; j0 < G::IPQ; j0 += NW) dma_rows_t(dQg, q0, (j0 + wave) * RPI, dq_lds);
   }
   if (nblk > 0) {
     dma_block(plan_block(plan, 0), st_lds);
@@ -362,18 +418,51 @@ void attn_mfma_kernel(const AttnArgs a) {
   // loads above are complete and does not wait for them inside the loop
   __builtin_amdgcn_s_waitcnt(0xF70);
   __syncthreads();
+  if constexpr (ZC) {
+    if (q0 < t0) {  // the tile straddles t0: its rows below t0 have zero dQ
+      zero_rows(sdQ, t0 - q0);
+      __syncthreads();
+    }
+  }
 
   int it = 0;
-  int cur = 0;  // stage of block it
-  while (it < nblk) {
+  int cur = 0;       // stage of block it
+  int cleared = -1;  // (kZeroClean) last block whose tangent rows below t0 were cleared
+  for (;;) {
     bool rescale = false;
-    while (it < nblk) {
-      const int nxt = cur == 0 ? 2 : cur - 1;  // (it + 2) mod 3
-      const char* cs = stages + cur * SB;
-      rescale = step(it, cs, cs + TB, cs + 2 * TB, cs + 2 * TB + TBJ, st_lds + (unsigned)(nxt * SB));
-      if (rescale) break;
-      ++it;
-      cur = cur == 2 ? 0 : cur + 1;
+    if constexpr (ZC) {
+      // key blocks below t0: no dK, dV terms
+      while (it < ntk) {
+        const int nxt = cur == 0 ? 2 : cur - 1;  // (it + 2) mod 3
+        const char* cs = stages + cur * SB;
+        rescale = step(Tag<false>{}, it, cs, cs + TB, cs + 2 * TB, cs + 2 * TB + TBJ,
+                       st_lds + (unsigned)(nxt * SB));
+        if (rescale) break;
+        ++it;
+        cur = cur == 2 ? 0 : cur + 1;
+      }
+    }
+    if (!rescale) {
+      while (it < nblk) {
+        const int nxt = cur == 0 ? 2 : cur - 1;  // (it + 2) mod 3
+        char* cs = stages + cur * SB;
+        if constexpr (ZC) {
+          // a block straddling t0: clear the tangent rows of its keys below t0 (once per
+          // block, so that every wave passes this barrier equally often)
+          const int k0 = plan_block(plan, it) * BC;
+          if (k0 < t0 && cleared != it) {
+            zero_rows(cs + 2 * TB, t0 - k0);
+            zero_rows(cs + 2 * TB + TBJ, t0 - k0);
+            asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+            cleared = it;
+          }
+        }
+        rescale = step(Tag<true>{}, it, cs, cs + TB, cs + 2 * TB, cs + 2 * TB + TBJ,
+                       st_lds + (unsigned)(nxt * SB));
+        if (rescale) break;
+        ++it;
+        cur = cur == 2 ? 0 : cur + 1;
+      }
     }
     if (!rescale) break;
     // Cold path: move the reference max of the rows that need it (lanes l and l^32 hold
@@ -402,7 +491,8 @@ void attn_mfma_kernel(const AttnArgs a) {
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   if (row < L) {
     bf16_t* Og = (bf16_t*)a.O + head + (size_t)row * D;
-    bf16_t* dOg = (bf16_t*)a.dO + head + (size_t)row * D;
+    bf16_t* dOg = (bf16_t*)a.dO + thead + (size_t)max(row - t0, 0) * D;
+    const bool store_do = !ZC || row >= t0;  // dO of rows below t0 is zero and not stored
 #pragma unroll
     for (int dt = 0; dt < G::DT; ++dt) {
 #pragma unroll
@@ -416,7 +506,9 @@ void attn_mfma_kernel(const AttnArgs a) {
           if constexpr (JVP) dov[e] = (bf16_t)((tacc[dt][4 * q4 + e] - r_tot * on) * inv);
         }
         *(bf16x4*)(Og + d) = ov;
-        if constexpr (JVP) *(bf16x4*)(dOg + d) = dov;
+        if constexpr (JVP) {
+          if (store_do) *(bf16x4*)(dOg + d) = dov;
+        }
       }
     }
     if (hh == 0)
@@ -424,17 +516,45 @@ void attn_mfma_kernel(const AttnArgs a) {
   }
 }
 
+template <int D, int MODE>
+__global__ __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_mfma_kernel(const AttnArgs a) {
+  constexpr bool JVP = MODE != kFwd;
+  using G = Geo<D>;
+  // LDS: three stages of K, V (+ dK, dV) tiles, and (JVP) the dQ tile of the query
+  // tile, read back as an MFMA operand (keeps the per-wave register footprint within
+  // two waves per SIMD).  D = 128 JVP: 3 x 32 KiB + 64 KiB = 160 KiB.
+  constexpr int SB = JVP ? 4 * G::TILEB : 2 * G::TILEB + 32;
+  __shared__ __attribute__((aligned(1024))) char stages[3 * SB];
+  __shared__ __attribute__((aligned(1024))) char sdQ[JVP ? BR * G::ROWB : 16];
+
+  const int nqt = a.order.nt;
+  const int bh = blockIdx.x / nqt;
+  const int qtile = tile_of(a.order, blockIdx.x - bh * nqt);
+  if constexpr (MODE == kZeroClean) {
+    if ((qtile + 1) * BR <= a.t0) {  // no tangent row in the tile: the primal only
+      tile_body<D, kFwd>(a, bh, qtile, stages, sdQ);
+      return;
+    }
+  }
+  tile_body<D, MODE>(a, bh, qtile, stages, sdQ);
+}
+
 }  // namespace
 
-hipError_t launch_mfma_bf16(const AttnArgs& a, int D, bool jvp, hipStream_t stream) {
+hipError_t launch_mfma_bf16(const AttnArgs& a, int D, Pass pass, hipStream_t stream) {
   const dim3 grid((unsigned)(a.order.nt * a.B * a.H));
   const dim3 block(NTHREADS);
   if (D == 128) {
-    if (jvp) hipLaunchKernelGGL((attn_mfma_kernel<128, true>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((attn_mfma_kernel<128, false>), grid, block, 0, stream, a);
+    if (pass == Pass::kJvp) hipLaunchKernelGGL((attn_mfma_kernel<128, kJvp>), grid, block, 0, stream, a);
+    else if (pass == Pass::kJvpZeroClean)
+      hipLaunchKernelGGL((attn_mfma_kernel<128, kZeroClean>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((attn_mfma_kernel<128, kFwd>), grid, block, 0, stream, a);
   } else {
-    if (jvp) hipLaunchKernelGGL((attn_mfma_kernel<64, true>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((attn_mfma_kernel<64, false>), grid, block, 0, stream, a);
+    if (pass == Pass::kJvp) hipLaunchKernelGGL((attn_mfma_kernel<64, kJvp>), grid, block, 0, stream, a);
+    else if (pass == Pass::kJvpZeroClean)
+      hipLaunchKernelGGL((attn_mfma_kernel<64, kZeroClean>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((attn_mfma_kernel<64, kFwd>), grid, block, 0, stream, a);
   }
   return hipGetLastError();
 }

@@ -8,6 +8,8 @@
 // skipping), with the online recurrence of the paper's Algorithm 1 (App. B) at
 // a block size of one key: running max m, normaliser l, accumulators O,
 // T = A + B and r, epilogue O / l, LSE = m + ln l, dO = (T - r O) / l.
+// When the tangents are zero below row t0 (and stored from row t0 on), rows
+// below t0 skip the tangent work and keys below t0 skip their dK, dV terms.
 #include <hip/hip_runtime.h>
 
 #include "kernels.hpp"
@@ -30,22 +32,27 @@ __global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_simt_kernel(const
   const int L = a.L;
   if (row >= L) return;  // whole wave leaves; no barriers below
 
+  // tangent rows are [t0, L) (t0 = 0 unless the rows below t0 carry zero tangents,
+  // which are then neither stored nor read)
+  const int t0 = a.t0;
   const size_t head = (size_t)bh * L * D;
+  const size_t thead = (size_t)bh * (L - t0) * D;
   const float* Q = (const float*)a.Q + head;
   const float* K = (const float*)a.K + head;
   const float* V = (const float*)a.V + head;
-  const float* dQ = (const float*)a.dQ + head;
-  const float* dK = (const float*)a.dK + head;
-  const float* dV = (const float*)a.dV + head;
+  const float* dQ = (const float*)a.dQ + thead;  // tangent row x - t0 of sequence row x
+  const float* dK = (const float*)a.dK + thead;
+  const float* dV = (const float*)a.dV + thead;
 
   const int g = find_group(a.gt, row);
   const int rng[2][2] = {{a.gt.a0[g], a.gt.a1[g]}, {a.gt.b0[g], a.gt.b1[g]}};
+  const bool row_tan = JVP && row >= t0;
 
   float q[E], dq[E], o[E], t[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     q[e] = Q[(size_t)row * D + lane + 64 * e];
-    dq[e] = JVP ? dQ[(size_t)row * D + lane + 64 * e] : 0.f;
+    dq[e] = row_tan ? dQ[(size_t)(row - t0) * D + lane + 64 * e] : 0.f;
     o[e] = 0.f;
     t[e] = 0.f;
   }
@@ -54,12 +61,13 @@ __global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_simt_kernel(const
 
   for (int ri = 0; ri < 2; ++ri) {
     for (int k = rng[ri][0]; k < rng[ri][1]; ++k) {
+      const bool key_tan = JVP && k >= t0;  // uniform across the wave
       float s = 0.f, ds = 0.f;
 #pragma unroll
       for (int e = 0; e < E; ++e) {
         const float kv = K[(size_t)k * D + lane + 64 * e];
         s += q[e] * kv;
-        if (JVP) ds += dq[e] * kv + q[e] * dK[(size_t)k * D + lane + 64 * e];
+        if (JVP) ds += dq[e] * kv + (key_tan ? q[e] * dK[(size_t)(k - t0) * D + lane + 64 * e] : 0.f);
       }
       s = wave_sum(s) * sc;
       if (JVP) ds = wave_sum(ds) * sc;
@@ -72,7 +80,7 @@ __global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_simt_kernel(const
       for (int e = 0; e < E; ++e) {
         const float vv = V[(size_t)k * D + lane + 64 * e];
         o[e] = o[e] * alpha + p * vv;
-        if (JVP) t[e] = t[e] * alpha + p * dV[(size_t)k * D + lane + 64 * e] + p * ds * vv;
+        if (JVP) t[e] = t[e] * alpha + (key_tan ? p * dV[(size_t)(k - t0) * D + lane + 64 * e] : 0.f) + p * ds * vv;
       }
       m = mnew;
     }
@@ -80,21 +88,21 @@ __global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_simt_kernel(const
 
   const float inv = l > 0.f ? 1.f / l : 0.f;
   float* O = (float*)a.O + head + (size_t)row * D;
-  float* dO = JVP ? (float*)a.dO + head + (size_t)row * D : nullptr;
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const float on = o[e] * inv;
     O[lane + 64 * e] = on;
-    if (JVP) dO[lane + 64 * e] = (t[e] - r * on) * inv;
+    if (row_tan) ((float*)a.dO + thead)[(size_t)(row - t0) * D + lane + 64 * e] = (t[e] - r * on) * inv;
   }
   if (lane == 0) a.LSE[(size_t)bh * L + row] = l > 0.f ? m + logf(l) : -INFINITY;
 }
 
 }  // namespace
 
-hipError_t launch_simt_f32(const AttnArgs& a, int D, bool jvp, hipStream_t stream) {
+hipError_t launch_simt_f32(const AttnArgs& a, int D, Pass pass, hipStream_t stream) {
   const dim3 grid((unsigned)((a.L + kSimtRowsPerBlock - 1) / kSimtRowsPerBlock), (unsigned)(a.B * a.H));
   const dim3 block(64 * kSimtRowsPerBlock);
+  const bool jvp = pass != Pass::kFwd;  // a.t0 selects the rows that carry tangents
   if (D == 128) {
     if (jvp) hipLaunchKernelGGL((attn_simt_kernel<128, true>), grid, block, 0, stream, a);
     else hipLaunchKernelGGL((attn_simt_kernel<128, false>), grid, block, 0, stream, a);

@@ -30,11 +30,15 @@ bool overlap(const Span& x, const Span& y) { return x.lo < y.hi && y.lo < x.hi; 
 
 int elem_size(int dtype) { return dtype == ATTN_DTYPE_F32 ? 4 : dtype == ATTN_DTYPE_BF16 ? 2 : 0; }
 
-// Shared validation of attn_jvp_fwd / attn_fwd; fills the launch arguments.
-int prepare(bool jvp, int dtype, int B, int H, int L, int D, const void* Q, const void* K,
+// Shared validation of the compute entry points; fills the launch arguments.
+// kJvpZeroClean: teacher-forcing layouts only; the tangents (and dO) hold the noisy
+// half, rows [L/2, L), of every (batch, head).
+int prepare(attn::Pass pass, int dtype, int B, int H, int L, int D, const void* Q, const void* K,
             const void* V, const void* dQ, const void* dK, const void* dV,
             const attn_chunk_layout* layout, float softmax_scale, void* O, void* dO, float* LSE,
             attn::AttnArgs* args) {
+  const bool jvp = pass != attn::Pass::kFwd;
+  const bool zc = pass == attn::Pass::kJvpZeroClean;
   if (dtype != ATTN_DTYPE_F32 && dtype != ATTN_DTYPE_BF16)
     return fail(ATTN_ERR_UNSUPPORTED, "unsupported dtype " + std::to_string(dtype));
   if (D != 64 && D != 128)
@@ -45,13 +49,19 @@ int prepare(bool jvp, int dtype, int B, int H, int L, int D, const void* Q, cons
   if ((int64_t)B * H > (int64_t)1 << 20) return fail(ATTN_ERR_INVALID, "B * H too large");
   if (!Q || !K || !V || !O || !LSE) return fail(ATTN_ERR_INVALID, "NULL tensor pointer");
   if (jvp && (!dQ || !dK || !dV || !dO)) return fail(ATTN_ERR_INVALID, "NULL tangent pointer");
+  if (!layout) return fail(ATTN_ERR_INVALID, "layout is NULL");
+  if (zc && layout->kind != ATTN_MASK_TEACHER_FORCING)
+    return fail(ATTN_ERR_INVALID, "the zero-clean-tangent JVP needs a teacher-forcing layout");
+  const int t0 = zc ? L / 2 : 0;
   const int es = elem_size(dtype);
   const uintptr_t tbytes = (uintptr_t)B * H * L * D * es;
+  const uintptr_t gbytes = (uintptr_t)B * H * (L - t0) * D * es;  // tangents and dO
   const uintptr_t lbytes = (uintptr_t)B * H * L * sizeof(float);
   const uintptr_t align = dtype == ATTN_DTYPE_BF16 ? 16 : 4;
   const void* ins[6] = {Q, K, V, dQ, dK, dV};
   const char* in_names[6] = {"Q", "K", "V", "dQ", "dK", "dV"};
-  for (int i = 0; i < (jvp ? 6 : 3); ++i)
+  const int nin = jvp ? 6 : 3;
+  for (int i = 0; i < nin; ++i)
     if ((uintptr_t)ins[i] % align)
       return fail(ATTN_ERR_INVALID, std::string(in_names[i]) + " is not " + std::to_string(align) +
                                         "-byte aligned");
@@ -59,14 +69,14 @@ int prepare(bool jvp, int dtype, int B, int H, int L, int D, const void* Q, cons
     return fail(ATTN_ERR_INVALID, "output pointer misaligned");
   Span outs[3] = {{(uintptr_t)O, (uintptr_t)O + tbytes, "O"},
                   {(uintptr_t)LSE, (uintptr_t)LSE + lbytes, "LSE"},
-                  {(uintptr_t)dO, (uintptr_t)dO + tbytes, "dO"}};
+                  {(uintptr_t)dO, (uintptr_t)dO + gbytes, "dO"}};
   const int nout = jvp ? 3 : 2;
   for (int i = 0; i < nout; ++i) {
     for (int j = i + 1; j < nout; ++j)
       if (overlap(outs[i], outs[j]))
         return fail(ATTN_ERR_INVALID, std::string("outputs ") + outs[i].name + " and " + outs[j].name + " overlap");
-    for (int k = 0; k < (jvp ? 6 : 3); ++k) {
-      const Span in = {(uintptr_t)ins[k], (uintptr_t)ins[k] + tbytes, in_names[k]};
+    for (int k = 0; k < nin; ++k) {
+      const Span in = {(uintptr_t)ins[k], (uintptr_t)ins[k] + (k < 3 ? tbytes : gbytes), in_names[k]};
       if (overlap(outs[i], in))
         return fail(ATTN_ERR_INVALID, std::string("output ") + outs[i].name + " overlaps input " + in.name);
     }
@@ -77,15 +87,17 @@ int prepare(bool jvp, int dtype, int B, int H, int L, int D, const void* Q, cons
   args->dQ = dQ; args->dK = dK; args->dV = dV;
   args->O = O; args->dO = dO; args->LSE = LSE;
   args->B = B; args->H = H; args->L = L;
+  args->t0 = t0;
   args->scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)D);
-  args->order = attn::make_tile_order(layout, L, attn::kMfmaBr);
+  args->order = zc ? attn::make_tile_order_zero_clean(args->gt, L, attn::kMfmaBr, attn::kMfmaBc, t0)
+                   : attn::make_tile_order(layout, L, attn::kMfmaBr);
   return ATTN_OK;
 }
 
-int launch(bool jvp, int dtype, int D, const attn::AttnArgs& args, void* stream) {
+int launch(attn::Pass pass, int dtype, int D, const attn::AttnArgs& args, void* stream) {
   const hipError_t e = dtype == ATTN_DTYPE_BF16
-                           ? attn::launch_mfma_bf16(args, D, jvp, (hipStream_t)stream)
-                           : attn::launch_simt_f32(args, D, jvp, (hipStream_t)stream);
+                           ? attn::launch_mfma_bf16(args, D, pass, (hipStream_t)stream)
+                           : attn::launch_simt_f32(args, D, pass, (hipStream_t)stream);
   if (e != hipSuccess) return fail(ATTN_ERR_HIP, std::string("HIP launch failed: ") + hipGetErrorString(e));
   return ATTN_OK;
 }
@@ -98,18 +110,30 @@ int attn_jvp_fwd(int dtype, int B, int H, int L, int D, const void* Q, const voi
                  const void* dQ, const void* dK, const void* dV, const attn_chunk_layout* layout,
                  float softmax_scale, void* O, void* dO, float* LSE, void* stream) {
   attn::AttnArgs args;
-  const int rc = prepare(true, dtype, B, H, L, D, Q, K, V, dQ, dK, dV, layout, softmax_scale, O, dO, LSE, &args);
+  const int rc = prepare(attn::Pass::kJvp, dtype, B, H, L, D, Q, K, V, dQ, dK, dV, layout, softmax_scale,
+                         O, dO, LSE, &args);
   if (rc != ATTN_OK) return rc;
-  return launch(true, dtype, D, args, stream);
+  return launch(attn::Pass::kJvp, dtype, D, args, stream);
+}
+
+int attn_jvp_fwd_zero_clean(int dtype, int B, int H, int L, int D, const void* Q, const void* K,
+                            const void* V, const void* dQn, const void* dKn, const void* dVn,
+                            const attn_chunk_layout* layout, float softmax_scale, void* O, void* dOn,
+                            float* LSE, void* stream) {
+  attn::AttnArgs args;
+  const int rc = prepare(attn::Pass::kJvpZeroClean, dtype, B, H, L, D, Q, K, V, dQn, dKn, dVn, layout,
+                         softmax_scale, O, dOn, LSE, &args);
+  if (rc != ATTN_OK) return rc;
+  return launch(attn::Pass::kJvpZeroClean, dtype, D, args, stream);
 }
 
 int attn_fwd(int dtype, int B, int H, int L, int D, const void* Q, const void* K, const void* V,
              const attn_chunk_layout* layout, float softmax_scale, void* O, float* LSE, void* stream) {
   attn::AttnArgs args;
-  const int rc = prepare(false, dtype, B, H, L, D, Q, K, V, nullptr, nullptr, nullptr, layout, softmax_scale,
-                         O, nullptr, LSE, &args);
+  const int rc = prepare(attn::Pass::kFwd, dtype, B, H, L, D, Q, K, V, nullptr, nullptr, nullptr, layout,
+                         softmax_scale, O, nullptr, LSE, &args);
   if (rc != ATTN_OK) return rc;
-  return launch(false, dtype, D, args, stream);
+  return launch(attn::Pass::kFwd, dtype, D, args, stream);
 }
 
 int64_t attn_count_unmasked_pairs(const attn_chunk_layout* layout, int L) {
@@ -172,6 +196,20 @@ int attn_tile_plan(const attn_chunk_layout* layout, int L, int qtile, int32_t* b
     full[i] = attn::block_is_full(p, blocks[i] * bc, bc, L) ? 1 : 0;
   }
   return nb;
+}
+
+int attn_tile_order(const attn_chunk_layout* layout, int L, int zero_clean, int32_t* order, int cap) {
+  attn::GroupTable gt;
+  std::string err;
+  if (!attn::build_groups(layout, L, &gt, &err)) return fail(ATTN_ERR_INVALID, err), -1;
+  if (zero_clean && layout->kind != ATTN_MASK_TEACHER_FORCING)
+    return fail(ATTN_ERR_INVALID, "the zero-clean-tangent JVP needs a teacher-forcing layout"), -1;
+  const attn::TileOrder o =
+      zero_clean ? attn::make_tile_order_zero_clean(gt, L, attn::kMfmaBr, attn::kMfmaBc, L / 2)
+                 : attn::make_tile_order(layout, L, attn::kMfmaBr);
+  if (!order || cap < o.nt) return fail(ATTN_ERR_INVALID, "output buffer too small"), -1;
+  for (int t = 0; t < o.nt; ++t) order[t] = attn::tile_of(o, t);
+  return o.nt;
 }
 
 const char* attn_last_error(void) { return g_last_error.c_str(); }

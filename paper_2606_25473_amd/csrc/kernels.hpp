@@ -20,6 +20,7 @@ struct AttnArgs {
   void* dO;
   float* LSE;
   int B, H, L;
+  int t0;           // tangent rows are [t0, L) (dQ, dK, dV, dO hold L - t0 rows per head)
   float scale;      // softmax scale s applied to scores and score tangents
   GroupTable gt;
   TileOrder order;
@@ -32,7 +33,11 @@ constexpr int kMfmaBc = 32;
 // fp32 exact-path kernels: one wave per query row.
 constexpr int kSimtRowsPerBlock = 4;
 
-hipError_t launch_mfma_bf16(const AttnArgs& a, int D, bool jvp, hipStream_t stream);
-hipError_t launch_simt_f32(const AttnArgs& a, int D, bool jvp, hipStream_t stream);
+// What a launch computes: the primal only, the JVP with tangents on every row (t0 = 0),
+// or the JVP whose tangents are zero on rows [0, t0) and stored for rows [t0, L) only.
+enum class Pass { kFwd, kJvp, kJvpZeroClean };
+
+hipError_t launch_mfma_bf16(const AttnArgs& a, int D, Pass pass, hipStream_t stream);
+hipError_t launch_simt_f32(const AttnArgs& a, int D, Pass pass, hipStream_t stream);
 
 }  // namespace attn

@@ -106,15 +106,62 @@ int64_t count_computed_pairs(const GroupTable& gt, int L, int br, int bc) {
 }
 
 TileOrder make_tile_order(const attn_chunk_layout* layout, int L, int br) {
-  TileOrder o;
+  TileOrder o{};
   o.nt = (L + br - 1) / br;
   o.split = o.nt;
+  o.first = -1;
   o.mode = 0;
   if (layout->kind == ATTN_MASK_BLOCK_CAUSAL) o.mode = 1;
   if (layout->kind == ATTN_MASK_TEACHER_FORCING) {
     o.mode = 2;
     const int half = L / 2;
     o.split = (half + br - 1) / br;  // the tile holding the clean/noisy boundary counts as clean
+  }
+  return o;
+}
+
+TileOrder make_tile_order_zero_clean(const GroupTable& gt, int L, int br, int bc, int t0) {
+  TileOrder o{};
+  o.nt = (L + br - 1) / br;
+  o.split = t0 / br;  // tiles wholly below t0 need the primal only; the boundary tile is upper
+  o.first = -1;
+  o.mode = 2;
+  const bool straddle = t0 % br != 0;
+  if (o.nt - (straddle ? 1 : 0) > kMaxMergeTiles) return o;  // merge bits for at most this many
+  // Cost of a tile in key-block contractions: 2 per block (scores, output) for a tile
+  // without tangent rows, 4 per block of keys without tangents (+ the dQ term of the
+  // score tangent and the H~ term of the output tangent), 6 per block with tangent keys.
+  auto cost = [&](int t) {
+    const int q0 = t * br, q1 = q0 + br < L ? q0 + br : L;
+    const TilePlan p = plan_tile(gt, q0, q1, bc);
+    const int nb = plan_num_blocks(p);
+    int64_t c = 0;
+    for (int i = 0; i < nb; ++i) {
+      const int k0 = plan_block(p, i) * bc;
+      c += q1 <= t0 ? 2 : (k0 + bc > t0 ? 6 : 4);
+    }
+    return c;
+  };
+  o.mode = 3;
+  // A tile straddling t0 holds the last clean chunk, which sees every clean key with
+  // the dQ term: one of the heaviest tiles, and out of place at the low end of the
+  // upper half.  It goes first.
+  int lo = o.split - 1, hi = o.nt - 1, stop = o.split;
+  if (straddle) {
+    o.first = o.split;
+    stop = o.split + 1;
+  }
+  int64_t clo = lo >= 0 ? cost(lo) : 0, chi = hi >= stop ? cost(hi) : 0;
+  for (int t = 0; t < o.nt - (o.first >= 0 ? 1 : 0); ++t) {
+    const bool take_hi = lo < 0 || (hi >= stop && chi >= clo);
+    if (take_hi) {
+      o.merge[t >> 5] |= 1u << (t & 31);
+      --hi;
+      chi = hi >= stop ? cost(hi) : 0;
+    } else {
+      --lo;
+      clo = lo >= 0 ? cost(lo) : 0;
+    }
   }
   return o;
 }

@@ -23,4 +23,9 @@ int64_t count_computed_pairs(const GroupTable& gt, int L, int br, int bc);
 // Work-group -> query-tile order for the layout (heaviest tiles first).
 TileOrder make_tile_order(const attn_chunk_layout* layout, int L, int br);
 
+// Tile order when the rows below t0 carry no tangent (their tiles need the primal
+// only): the tiles wholly below t0 and the others, each heaviest first, merged by
+// estimated cost (mode 3; mode 2 beyond kMaxMergeTiles tiles).
+TileOrder make_tile_order_zero_clean(const GroupTable& gt, int L, int br, int bc, int t0);
+
 }  // namespace attn

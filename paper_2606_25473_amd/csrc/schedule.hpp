@@ -122,9 +122,26 @@ ATTN_HD bool block_is_full(const TilePlan& p, int k0, int bc, int L) {
 //   mode 2: two halves [0, split) and [split, nt), each taken from its end,
 //           interleaved (teacher forcing: work grows with the chunk index in
 //           both the clean and the noisy half)
+//   mode 3: tile `first` (if >= 0; it is then tile `split`), followed by the two
+//           halves [0, split) and [split + (first >= 0), nt), each taken from its
+//           end and merged by the bit string `merge` (bit t set: the t-th tile after
+//           `first` is the next one of the upper half).  The host merges by
+//           estimated tile cost, for layouts whose halves cost different amounts
+//           per tile.
+constexpr int kMaxMergeTiles = 1024;
+
 struct TileOrder {
-  int mode, nt, split;
+  int mode, nt, split, first;
+  uint32_t merge[kMaxMergeTiles / 32];
 };
+
+ATTN_HD int popc32(uint32_t x) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __popc(x);
+#else
+  return __builtin_popcount(x);
+#endif
+}
 
 ATTN_HD int tile_of(const TileOrder& o, int t) {
   if (o.mode == 1) return o.nt - 1 - t;
@@ -134,6 +151,17 @@ ATTN_HD int tile_of(const TileOrder& o, int t) {
     if (t < 2 * m) return (t & 1) ? (o.nt - 1 - (t >> 1)) : (na - 1 - (t >> 1));
     const int r = t - 2 * m;
     return na > nb ? (na - 1 - m - r) : (o.nt - 1 - m - r);
+  }
+  if (o.mode == 3) {
+    if (o.first >= 0) {
+      if (t == 0) return o.first;
+      --t;
+    }
+    int upper = 0;  // upper-half tiles taken before position t
+    for (int w = 0; w < (t >> 5); ++w) upper += popc32(o.merge[w]);
+    const uint32_t word = o.merge[t >> 5];
+    upper += popc32(word & ((1u << (t & 31)) - 1u));
+    return ((word >> (t & 31)) & 1u) ? o.nt - 1 - upper : o.split - 1 - (t - upper);
   }
   return t;
 }

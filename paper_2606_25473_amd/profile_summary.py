@@ -1,7 +1,7 @@
 """Summarise rocprofv3 CSV output of a bench.py run into a short text report.
 
     python -m paper_2606_25473_amd.profile_summary --trace DIR [--fetch DIR --write DIR]
-        [--copy-mib N] [--workload NAME] [--op jvp|fwd] [--record profiles/hbm_traffic.json]
+        [--copy-mib N] [--workload NAME] [--op jvp|fwd|zc] [--record profiles/hbm_traffic.json]
 
 --trace: a ``rocprofv3 --kernel-trace --stats -f csv`` output directory;
 --fetch/--write: ``rocprofv3 --pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE`` output
@@ -59,7 +59,7 @@ def main(argv=None):
     ap.add_argument("--write")
     ap.add_argument("--copy-mib", type=int, default=0)
     ap.add_argument("--workload", default="wan1.3b_chunkwise_tf")
-    ap.add_argument("--op", default="jvp", choices=["jvp", "fwd"])
+    ap.add_argument("--op", default="jvp", choices=["jvp", "fwd", "zc"])
     ap.add_argument("--record")
     ap.add_argument("--pmc", nargs="*", default=[], help="counter-collection output dirs to list")
     a = ap.parse_args(argv)

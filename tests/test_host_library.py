@@ -135,6 +135,47 @@ def test_computed_pair_overhead_on_wan_chunkwise(lib):
     assert 1.0 <= comp / un < 1.02
 
 
+def _tile_cost(kind, offsets, L, t, zero_clean):
+    """Key-block contractions of tile t: 2 (scores, output) per block for a primal-only
+    tile, 4 per block of clean keys and 6 per block with noisy keys otherwise."""
+    R, C = binding.tile_shape()
+    half = L // 2
+    blocks = [b for b, _ in binding.tile_plan(kind, offsets, L, t)]
+    if not zero_clean:
+        return 6 * len(blocks)
+    if (t + 1) * R <= half:
+        return 2 * len(blocks)
+    return sum(6 if b * C + C > half else 4 for b in blocks)
+
+
+@pytest.mark.parametrize("kind,offsets,L", LAYOUTS)
+def test_tile_order_is_a_permutation(lib, kind, offsets, L):
+    R, _ = binding.tile_shape()
+    nt = (L + R - 1) // R
+    assert sorted(binding.tile_order(kind, offsets, L)) == list(range(nt))
+    if kind == MASK_TEACHER_FORCING:
+        assert sorted(binding.tile_order(kind, offsets, L, zero_clean=True)) == list(range(nt))
+
+
+@pytest.mark.parametrize("name", ["wan1.3b_chunkwise_tf", "wan1.3b_framewise_tf"])
+def test_zero_clean_tile_order_is_heaviest_first(lib, name):
+    """The zero-clean order starts with one of the heaviest tiles and ends with the
+    lightest ones: every tile of the last quarter costs at most what the lightest
+    tile of the first quarter costs (the tiles straddling two noisy chunks are the
+    only ones out of monotone order, and only slightly)."""
+    w = WORKLOADS[name]
+    order = binding.tile_order(w.kind, w.offsets, w.L, zero_clean=True)
+    costs = [_tile_cost(w.kind, w.offsets, w.L, t, True) for t in order]
+    q = len(costs) // 4
+    assert costs[0] >= 0.9 * max(costs) and costs[-1] == min(costs)
+    assert max(costs[-q:]) <= min(costs[:q])
+
+
+def test_tile_order_rejects_zero_clean_without_teacher_forcing(lib):
+    with pytest.raises(binding.AttnError):
+        binding.tile_order("block_causal", [0, 300, 600], 600, zero_clean=True)
+
+
 # ----------------------------------------------------------------------------- error paths
 
 FAKE = 1 << 40          # never dereferenced: every call below fails validation first
@@ -193,6 +234,30 @@ def test_invalid_arguments_are_rejected_before_any_hip_call(lib, kw, code, needl
     rc = _call(lib, **kw)
     assert rc == code
     assert needle in binding.last_error()
+
+
+@_no_gpu
+def test_zero_clean_entry_point_validates(lib):
+    # tangents of the noisy half: [1, 1, 32, 64] bf16 buffers
+    p = _ptrs(9)
+    lay = make_layout("full")
+    rc = lib.attn_jvp_fwd_zero_clean(1, 1, 1, 64, 64, p[0], p[1], p[2], p[3], p[4], p[5], ctypes.byref(lay),
+                                     0.0, p[6], p[7], p[8], None)
+    assert rc == 1 and "teacher-forcing" in binding.last_error()
+    lay = make_layout("teacher_forcing", [0, 16, 32])
+    # dOn overlapping dKn (both are half-length buffers: 4096 bytes)
+    q = list(p)
+    q[7] = q[4] + 2048
+    rc = lib.attn_jvp_fwd_zero_clean(1, 1, 1, 64, 64, q[0], q[1], q[2], q[3], q[4], q[5], ctypes.byref(lay),
+                                     0.0, q[6], q[7], q[8], None)
+    assert rc == 1 and "overlaps input dK" in binding.last_error()
+    # a dOn right after a half-length dKn does not overlap it (the buffers are half-length);
+    # a layout error is then the first failure
+    q[7] = q[4] + 4096
+    rc = lib.attn_jvp_fwd_zero_clean(1, 1, 1, 64, 64, q[0], q[1], q[2], q[3], q[4], q[5],
+                                     ctypes.byref(make_layout("teacher_forcing", [0, 16, 40])), 0.0,
+                                     q[6], q[7], q[8], None)
+    assert rc == 1 and "L = 2" in binding.last_error()
 
 
 @_no_gpu

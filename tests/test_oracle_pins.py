@@ -18,7 +18,7 @@ import torch.nn.functional as F
 from torch.nn.attention import SDPBackend, sdpa_kernel
 
 from oracle import (MASK_BLOCK_CAUSAL, MASK_FULL, MASK_RANGES, MASK_TEACHER_FORCING, allowed_mask,
-                    attention_fwd, attention_jvp, count_allowed_pairs)
+                    attention_fwd, attention_jvp, attention_jvp_zero_clean, count_allowed_pairs)
 from oracle.dual import attention_dual
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -323,3 +323,49 @@ def test_row_subset_matches_full_evaluation():
     np.testing.assert_allclose(Os, O[:, :, rows], rtol=1e-13, atol=1e-14)
     np.testing.assert_allclose(dOs, dO[:, :, rows], rtol=1e-13, atol=1e-14)
     np.testing.assert_allclose(LSEs, LSE[:, :, rows], rtol=1e-14, atol=1e-14)
+
+
+# ----------------------------------------------------------------------------- zero clean tangents
+
+@pytest.mark.parametrize("N,C", [(3, 4), (4, 3), (1, 5)])
+def test_zero_clean_tangent_vs_torch_jvp(N, C):
+    """Paper Sec. 3.1.2 (TF-sCM tangent [0^clean, t^noisy]): clean rows have dO = 0
+    exactly, and noisy chunk i equals torch's JVP of dense attention over
+    [clean chunks < i | noisy chunk i] with zero tangents on the clean keys."""
+    B, H, D = 1, 2, 8
+    half = N * C
+    L = 2 * half
+    q, k, v = [torch.from_numpy(_rand((B, H, L, D), 130 + s)) for s in range(3)]
+    dqn, dkn, dvn = [torch.from_numpy(_rand((B, H, half, D), 140 + s)) for s in range(3)]
+    O, dO, LSE = attention_jvp_zero_clean(q.numpy(), k.numpy(), v.numpy(), dqn.numpy(), dkn.numpy(),
+                                          dvn.numpy(), _tf(N, C))
+    assert dO.shape == (B, H, L, D)
+    assert np.all(dO[:, :, :half] == 0.0)
+    O_fwd, LSE_fwd = attention_fwd(q.numpy(), k.numpy(), v.numpy(), MASK_TEACHER_FORCING, _tf(N, C))
+    np.testing.assert_array_equal(O, O_fwd)
+    np.testing.assert_array_equal(LSE, LSE_fwd)
+    z = torch.zeros(B, H, half, D, dtype=torch.float64)
+    dq, dk, dv = [torch.cat([z, t], dim=2) for t in (dqn, dkn, dvn)]
+    for i in range(N):
+        q_sl = slice(half + i * C, half + (i + 1) * C)
+        keys = torch.cat([torch.arange(0, i * C), torch.arange(half + i * C, half + (i + 1) * C)])
+        o2, do2 = _torch_jvp(q[:, :, q_sl], k[:, :, keys], v[:, :, keys],
+                             dq[:, :, q_sl], dk[:, :, keys], dv[:, :, keys])
+        np.testing.assert_allclose(O[:, :, q_sl], o2.numpy(), rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(dO[:, :, q_sl], do2.numpy(), rtol=1e-11, atol=1e-12)
+
+
+def test_zero_clean_tangent_noisy_rows_drop_clean_key_terms():
+    """Over clean keys only the dQ term of the score tangent and the V term of the
+    output tangent survive: perturbing the clean part of padded dK, dV changes the
+    noisy dO, while the zero-clean JVP is blind to it by construction."""
+    (Q, K, V, dQ, dK, dV), offs = _tf_inputs()
+    half = Q.shape[2] // 2
+    O, dO, _ = attention_jvp_zero_clean(Q, K, V, dQ[:, :, half:], dK[:, :, half:], dV[:, :, half:], offs)
+    X = [a.copy() for a in (dQ, dK, dV)]
+    for a in X:
+        a[:, :, :half] = 0.0
+    _, dO_pad, _ = attention_jvp(Q, K, V, *X, MASK_TEACHER_FORCING, offs)
+    np.testing.assert_array_equal(dO, dO_pad)
+    _, dO_dense, _ = attention_jvp(Q, K, V, dQ, dK, dV, MASK_TEACHER_FORCING, offs)
+    assert _rel(dO[:, :, half:], dO_dense[:, :, half:]) > 1e-3   # the clean tangents did matter
