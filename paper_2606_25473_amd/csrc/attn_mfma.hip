@@ -294,15 +294,56 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   const float sc = a.scale;
   const int krow = lane & 31;
 
-  // End of an iteration: wait until every load but this iteration's prefetch (N per
-  // wave) has landed -- so the next block is complete -- and every LDS read has
-  // returned, then synchronise the work-group.  D = 128: every wave issues one load per
-  // tile; D = 64: waves 0..3 do and the others issue none (nothing outstanding).
+  // Two schedules of the key-block loop, both with three LDS stages.
+  //
+  // Lockstep (the dense JVP): every wave passes the barrier of block k after both
+  // phases of block k.  Block k+2 streams into stage (k+2) mod 3 during iterations k
+  // and k+1 (two iterations of latency hidden).
+  //
+  // Ping-pong (forward-only and zero-clean kernels, whose share of softmax work is
+  // larger): the waves of the first half of the work-group (one per SIMD) pass the
+  // barrier of block k after its output phase, those of the second half after its
+  // score phase, so that each SIMD runs one wave's score phase (MFMA, then the softmax
+  // on the vector ALU) beside the other wave's output phase:
+  //   interval k (from barrier k-1 to barrier k):  first half   S(k), O(k)
+  //                                                 second half  O(k-1), S(k)
+  // Stage k mod 3 is then read in intervals k and k+1, so block k+1 streams into stage
+  // (k+1) mod 3 (whose block, k-2, was last read in interval k-1) during interval k
+  // only.  The score phase runs at raised wave priority, so that its MFMAs go first and
+  // its softmax overlaps the other wave's output MFMAs.
+  constexpr bool PP = MODE != kJvp;
+  constexpr int DIST = PP ? 1 : 2;  // prefetch distance in blocks
+  const bool late = PP && wave >= NW / 2;
+  // barrier of block k: every own load but those of block k+DIST has landed (lockstep:
+  // N per wave; D = 128: one per tile and wave; D = 64: waves 0..3 issue one, the others
+  // none), every LDS read has returned
   auto end_iteration = [&]() {
-    constexpr int N = (JVP ? 4 : 2) * ((G::IPT + NW - 1) / NW);
-    static_assert(N == 2 || N == 4, "vmcnt immediate below");
+    constexpr int N = PP ? 0 : (JVP ? 4 : 2) * ((G::IPT + NW - 1) / NW);
+    static_assert(N == 0 || N == 4, "vmcnt immediate below");
     if constexpr (N == 4) asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    else asm volatile("s_waitcnt vmcnt(2) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  };
+
+  // Output phase of a block: O^T += V^T P~^T ; T^T += dV^T P~^T + V^T H~^T
+  auto ophase = [&](auto tk, const char* cV, const char* cdV, const bf16x8* pb, const bf16x8* hb) {
+    constexpr bool TK = JVP && decltype(tk)::value;
+    // ---- O^T += V^T P~^T ; T^T += dV^T P~^T + V^T H~^T
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+#pragma unroll
+      for (int dt = 0; dt < G::DT; ++dt) {
+        const bf16x8 vop = cat(ld_tr(cV + tro[t][0][dt]), ld_tr(cV + tro[t][1][dt]));
+        oacc[dt] = mfma(vop, pb[t], oacc[dt]);
+        if constexpr (JVP) {
+          if constexpr (TK) {
+            const bf16x8 dvop = cat(ld_tr(cdV + tro[t][0][dt]), ld_tr(cdV + tro[t][1][dt]));
+            tacc[dt] = mfma(dvop, pb[t], tacc[dt]);
+          }
+          tacc[dt] = mfma(vop, hb[t], tacc[dt]);
+        }
+      }
+    }
+
   };
 
   // One key block; TK: the block has tangent keys (dK, dV tiles are present).  Returns
@@ -311,12 +352,18 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   auto step = [&](auto tk, int it, const char* cK, const char* cV, const char* cdK, const char* cdV,
                   unsigned next_stage) -> bool {
     constexpr bool TK = JVP && decltype(tk)::value;
-    // prefetch block it+2 into the stage freed by block it-1: a fixed number of loads
-    // per iteration (indices past the end are clamped; that stage is never read)
-    dma_block(plan_block(plan, min(it + 2, nblk - 1)), next_stage);
+    // prefetch block it+DIST (redone, with the same data, when the block is redone).
+    // Lockstep: a fixed number of loads per iteration, indices past the end clamped (that
+    // stage is never read).
+    if constexpr (PP) {
+      if (it + 1 < nblk) dma_block(plan_block(plan, it + 1), next_stage);
+    } else {
+      dma_block(plan_block(plan, min(it + 2, nblk - 1)), next_stage);
+    }
     const int k0 = plan_block(plan, it) * BC;
 
     // ---- scores and score tangents (transposed): S^T = K Q^T, dS^T = dK Q^T + K dQ^T
+    if constexpr (PP) __builtin_amdgcn_s_setprio(1);
     f32x16 S = f32x16{}, dS = f32x16{};
 #pragma unroll
     for (int s = 0; s < G::KS; ++s) {
@@ -367,43 +414,28 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
       p[i] = __builtin_amdgcn_exp2f(fmaf(sv[i], c2, mneg));
       lsum += p[i];
     }
-    float hv[16];
+    bf16x8 pb[2], hb[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) pb[t][j] = (bf16_t)p[8 * t + j];
     if constexpr (JVP) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        hv[i] = p[i] * (dsv[i] * sc);
-        rsum += hv[i];
+        const float hv = p[i] * (dsv[i] * sc);
+        rsum += hv;
+        hb[i >> 3][i & 7] = (bf16_t)hv;
       }
     }
 
-    // ---- O^T += V^T P~^T ; T^T += dV^T P~^T + V^T H~^T
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      bf16x8 pb, hb;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        pb[j] = (bf16_t)p[8 * t + j];
-        if constexpr (JVP) hb[j] = (bf16_t)hv[8 * t + j];
-      }
-#pragma unroll
-      for (int dt = 0; dt < G::DT; ++dt) {
-        const bf16x8 vop = cat(ld_tr(cV + tro[t][0][dt]), ld_tr(cV + tro[t][1][dt]));
-        oacc[dt] = mfma(vop, pb, oacc[dt]);
-        if constexpr (JVP) {
-          if constexpr (TK) {
-            const bf16x8 dvop = cat(ld_tr(cdV + tro[t][0][dt]), ld_tr(cdV + tro[t][1][dt]));
-            tacc[dt] = mfma(dvop, pb, tacc[dt]);
-          }
-          tacc[dt] = mfma(vop, hb, tacc[dt]);
-        }
-      }
-    }
-
-    end_iteration();  // block it+1 is in for every wave; nobody reads stage `it` any more
+    if constexpr (PP) __builtin_amdgcn_s_setprio(0);
+    if (late) end_iteration();
+    ophase(tk, cV, cdV, pb, hb);
+    if (!late) end_iteration();
     return false;
   };
 
-  // prologue: dQ of the query tile, then the first two key blocks
+  // prologue: dQ of the query tile, then the first DIST key blocks
   const unsigned st_lds = __builtin_amdgcn_readfirstlane(lds_addr(stages));
   if constexpr (JVP) {
     const unsigned dq_lds = __builtin_amdgcn_readfirstlane(lds_addr(sdQ));
@@ -412,7 +444,7 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   }
   if (nblk > 0) {
     dma_block(plan_block(plan, 0), st_lds);
-    dma_block(plan_block(plan, min(1, nblk - 1)), st_lds + SB);
+    if constexpr (!PP) dma_block(plan_block(plan, min(1, nblk - 1)), st_lds + SB);
   }
   // vmcnt(0) through the builtin, so that the compiler also knows that the Q operand
   // loads above are complete and does not wait for them inside the loop
@@ -433,7 +465,7 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
     if constexpr (ZC) {
       // key blocks below t0: no dK, dV terms
       while (it < ntk) {
-        const int nxt = cur == 0 ? 2 : cur - 1;  // (it + 2) mod 3
+        const int nxt = PP ? (cur == 2 ? 0 : cur + 1) : (cur == 0 ? 2 : cur - 1);  // (it + DIST) mod 3
         const char* cs = stages + cur * SB;
         rescale = step(Tag<false>{}, it, cs, cs + TB, cs + 2 * TB, cs + 2 * TB + TBJ,
                        st_lds + (unsigned)(nxt * SB));
@@ -444,7 +476,7 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
     }
     if (!rescale) {
       while (it < nblk) {
-        const int nxt = cur == 0 ? 2 : cur - 1;  // (it + 2) mod 3
+        const int nxt = PP ? (cur == 2 ? 0 : cur + 1) : (cur == 0 ? 2 : cur - 1);  // (it + DIST) mod 3
         char* cs = stages + cur * SB;
         if constexpr (ZC) {
           // a block straddling t0: clear the tangent rows of its keys below t0 (once per
@@ -468,7 +500,7 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
     // Cold path: move the reference max of the rows that need it (lanes l and l^32 hold
     // the same query, so the new reference is their joint max), rescale O, T, l, r, and
     // redo block `it` (its S is recomputed; its stage still holds its K/V, and the
-    // repeated prefetch rewrites stage (it+2) mod 3 with identical data).
+    // repeated prefetch rewrites stage (it+1) mod 3 with identical data).
     const float mx = fmaxf(mpend, xor32(mpend));
     const bool up = mx > m + kLazy;
     const float mnew = up ? mx : m;
@@ -482,8 +514,6 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
     }
     m = mnew;
   }
-
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the clamped tail prefetches have landed
 
   // ---- epilogue: combine the two half-waves' partial sums, normalise, store
   const float l_tot = lsum + xor32(lsum);

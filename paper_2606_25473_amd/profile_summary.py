@@ -16,9 +16,17 @@ import csv
 import glob
 import json
 import os
+import re
 import statistics
 
-ATTN = "attn_mfma_kernel"
+# template mode of attn_mfma_kernel<D, mode> for each op
+OP_MODE = {"fwd": 0, "jvp": 1, "zc": 2}
+
+
+def attn_kernel_of(op):
+    """Predicate on rocprofv3 kernel names selecting the bf16 kernel of ``op``."""
+    pat = re.compile(r"attn_mfma_kernel<\d+, %d>" % OP_MODE[op])
+    return lambda name: bool(pat.search(name))
 
 
 def _rows(d, suffix):
@@ -46,8 +54,9 @@ def counter_per_dispatch(d, counter):
 
 
 def _pick(d, key):
+    """First (name, values) whose name contains ``key`` (a string) or satisfies it (a predicate)."""
     for name, vals in d.items():
-        if key in name:
+        if (key(name) if callable(key) else key in name):
             return name, vals
     return None, []
 
@@ -78,7 +87,7 @@ def main(argv=None):
             per = counter_per_dispatch(d, cnt)
             # the calibration copy is a device-to-device hipMemcpy (runtime blit kernel)
             cname, cvals = _pick(per, "copyBuffer")
-            kname, kvals = _pick(per, ATTN)
+            kname, kvals = _pick(per, attn_kernel_of(a.op))
             if not cvals or not kvals:
                 lines.append(f"{cnt}: copy or attention kernel missing in {d}")
                 continue
@@ -94,10 +103,11 @@ def main(argv=None):
             lines.append(f"HBM traffic per launch: {traffic / 1e9:.3f} GB "
                          f"(read {out['read'] / 1e9:.3f} + write {out['write'] / 1e9:.3f})")
     derived = {}
+    is_attn = attn_kernel_of(a.op)
     for d in a.pmc:
         per, dur = {}, []
         for r in _rows(d, "counter_collection.csv"):
-            if ATTN in r["Kernel_Name"]:
+            if is_attn(r["Kernel_Name"]):
                 per.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
                 if r["Counter_Name"] == "GRBM_GUI_ACTIVE":
                     dur.append(float(r["End_Timestamp"]) - float(r["Start_Timestamp"]))
