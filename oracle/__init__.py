@@ -14,6 +14,8 @@ attention  -- closed-form masked attention O, LSE and the forward-mode tangent
               dO (paper, App. B, the masked-attention and tangent equations),
               and the same JVP with zero tangents on the clean half of a
               teacher-forcing sequence (paper Sec. 3.1.2, TF-sCM tangent).
+backward   -- the closed-form gradient (vector-Jacobian product) of the same
+              masked attention: gQ, gK, gV and Delta = rowsum(gO o O).
 dual       -- a pure-Python dual-number evaluation of the same map, used on
               tiny inputs to pin the closed form (no closed-form tangent used).
 
@@ -24,8 +26,10 @@ hand-derived golden values and invariants).
 """
 from .masks import MASK_FULL, MASK_BLOCK_CAUSAL, MASK_TEACHER_FORCING, MASK_RANGES, allowed_mask, count_allowed_pairs
 from .attention import attention_jvp, attention_fwd, attention_jvp_zero_clean
+from .backward import attention_vjp
 
 __all__ = [
     "MASK_FULL", "MASK_BLOCK_CAUSAL", "MASK_TEACHER_FORCING", "MASK_RANGES",
     "allowed_mask", "count_allowed_pairs", "attention_jvp", "attention_fwd", "attention_jvp_zero_clean",
+    "attention_vjp",
 ]
