@@ -1,7 +1,7 @@
 """Throughput of the fused masked attention forward + JVP on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--forward | --zero-clean]
-                    [--no-cpu]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                    [--forward | --zero-clean | --backward] [--no-cpu]
 
 One step = one ``attn_jvp_fwd`` call over the whole batch of the workload
 (default: Wan2.1-1.3B chunk-wise teacher forcing, B=1, H=12, L=65520, D=128,
@@ -11,7 +11,10 @@ bf16), inputs already resident in HBM.  Work is counted over admissible
 workloads: tangents of the noisy half only) and counts the work that variant
 must do: 4*D per pair of a clean query, 8*D per (noisy query, clean key) pair
 (scores, dQ term, output, H~ term), 12*D per (noisy query, noisy key) pair; it
-also reports the dense JVP's time on the same inputs.
+also reports the dense JVP's time on the same inputs.  ``--backward`` times
+``attn_bwd`` (both of its launches) for a cotangent gO, with O and LSE from an
+untimed ``attn_fwd``, and counts 10*D flop per pair (scores recomputed, gP, gV,
+gK, gQ).
 Prints ONE JSON line.  The ``cpu_baseline`` leg times the fp64 CPU oracle on a
 bounded sample of query rows of the same workload (and checks the sampled GPU
 rows against it).
@@ -29,8 +32,8 @@ import torch
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from paper_2606_25473_amd import (attn_fwd, attn_jvp_fwd, attn_jvp_fwd_zero_clean, count_computed_pairs,  # noqa: E402
-                                  count_unmasked_pairs, query_groups)
+from paper_2606_25473_amd import (attn_bwd, attn_fwd, attn_jvp_fwd, attn_jvp_fwd_zero_clean,  # noqa: E402
+                                  count_computed_pairs, count_unmasked_pairs, query_groups)
 from paper_2606_25473_amd.workloads import HEADLINE, WORKLOADS, make_inputs  # noqa: E402
 
 METRIC = "masked attention fwd+JVP TFLOP/s (unmasked pairs) and % bf16 MFMA peak"
@@ -145,6 +148,38 @@ def cpu_baseline(w, x, out, mode, budget_s=15.0):
             "sample_rel_l2_vs_gpu": rel}
 
 
+def cpu_baseline_bwd(w, x, out, budget_s=15.0):
+    """Time the fp64 backward oracle on a bounded sample of query rows (gQ) of head (0, 0)."""
+    from oracle import allowed_mask, attention_vjp  # the oracle is only used on this leg
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        cores = int(blas[0]["num_threads"]) if blas else os.cpu_count()
+    except Exception:
+        cores = os.cpu_count()
+    L, D = w.L, w.D
+    h = {k: v[0:1, 0:1].float().cpu().numpy() for k, v in x.items()}
+    offs = list(w.offsets) or None
+    order = np.random.default_rng(0).permutation(L)
+    done, t_used, pairs, errs = 0, 0.0, 0, []
+    empty = np.array([], dtype=np.int64)
+    while t_used < budget_s and done < L:
+        rows = np.sort(order[done:done + 256])
+        t0 = time.perf_counter()
+        gQ, _, _, _ = attention_vjp(h["Q"], h["K"], h["V"], h["gO"], w.kind, offs, rows=rows, keys=empty)
+        t_used += time.perf_counter() - t0
+        done += len(rows)
+        pairs += int(allowed_mask(w.kind, offs, L, rows).sum())
+        g = out[0][0, 0].index_select(0, torch.from_numpy(rows).to(out[0].device)).float().cpu().numpy()
+        errs.append((np.linalg.norm(g - gQ[0, 0]) ** 2, np.linalg.norm(gQ[0, 0]) ** 2))
+    rel = float(np.sqrt(sum(e for e, _ in errs) / max(sum(n for _, n in errs), 1e-300)))
+    # per pair the oracle evaluates the same five contractions (10 D flop) as the metric counts
+    return {"value": pairs * 10 * D / t_used / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": f"gQ of {done} query rows of head (0,0) spread over the {L}-token sequence "
+                      f"({pairs} admissible pairs, {t_used:.1f} s, fp64 numpy)",
+            "sample_rel_l2_vs_gpu": rel}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -154,6 +189,7 @@ def main():
     ap.add_argument("--forward", action="store_true", help="time attn_fwd instead of attn_jvp_fwd")
     ap.add_argument("--zero-clean", action="store_true",
                     help="time attn_jvp_fwd_zero_clean (teacher forcing, zero clean-half tangents)")
+    ap.add_argument("--backward", action="store_true", help="time attn_bwd (gradients for a cotangent of O)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -168,11 +204,11 @@ def main():
         sys.exit(1)
 
     w = WORKLOADS[args.workload]
-    if args.forward and args.zero_clean:
-        ap.error("--forward and --zero-clean are exclusive")
+    if args.forward + args.zero_clean + args.backward > 1:
+        ap.error("--forward, --zero-clean and --backward are exclusive")
     if args.zero_clean and w.kind != "teacher_forcing":
         ap.error("--zero-clean needs a teacher-forcing workload")
-    mode = "fwd" if args.forward else ("zc" if args.zero_clean else "jvp")
+    mode = "fwd" if args.forward else ("zc" if args.zero_clean else ("bwd" if args.backward else "jvp"))
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     x = make_inputs(w, "cuda", seed=0)
@@ -189,12 +225,23 @@ def main():
         dqn, dkn, dvn = x["dQn"], x["dKn"], x["dVn"]
         del dq, dk, dv
         don = torch.empty_like(dqn)
+    if mode == "bwd":  # cotangent: the dV draw; O and LSE from the forward (untimed)
+        go = x.pop("dV")
+        for n in ("dQ", "dK"):
+            del x[n]
+        del dq, dk, dv
+        x["gO"] = go
+        attn_fwd(q, k, v, w.kind, offs, out=(o, lse))
+        gq, gk, gv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+        delta = torch.empty_like(lse)
 
     def step():
         if mode == "fwd":
             attn_fwd(q, k, v, w.kind, offs, out=(o, lse))
         elif mode == "zc":
             attn_jvp_fwd_zero_clean(q, k, v, dqn, dkn, dvn, offs, out=(o, don, lse))
+        elif mode == "bwd":
+            attn_bwd(q, k, v, o, go, lse, w.kind, offs, out=(gq, gk, gv, delta))
         else:
             attn_jvp_fwd(q, k, v, dq, dk, dv, w.kind, offs, out=(o, do, lse))
 
@@ -228,7 +275,7 @@ def main():
     if mode == "zc":
         flop = zero_clean_flop(query_groups(w.kind, offs, L), half, D) * B * H
     else:
-        flop = pairs * (4 if mode == "fwd" else 12) * D * B * H
+        flop = pairs * {"fwd": 4, "bwd": 10, "jvp": 12}[mode] * D * B * H
     value = flop / (ms_per_step * 1e-3) / 1e12
     achieved = flop / (kernel_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_TFLOPS
@@ -247,7 +294,8 @@ def main():
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic",
-        "config": dict(w.describe(), op={"fwd": "attn_fwd", "zc": "attn_jvp_fwd_zero_clean"}.get(mode, "attn_jvp_fwd")),
+        "config": dict(w.describe(), op={"fwd": "attn_fwd", "zc": "attn_jvp_fwd_zero_clean",
+                                         "bwd": "attn_bwd"}.get(mode, "attn_jvp_fwd")),
         "pct_peak": round(100 * achieved / peak, 2),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": round(peak, 1),
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
@@ -282,8 +330,10 @@ def main():
         del pad, o2, do2
         step()  # restore the outputs the CPU leg compares against
         torch.cuda.synchronize()
-    if not args.no_cpu:
+    if not args.no_cpu and mode != "bwd":
         res["cpu_baseline"] = cpu_baseline(w, x, (o, don if mode == "zc" else do, lse), mode, args.cpu_budget)
+    if not args.no_cpu and mode == "bwd":
+        res["cpu_baseline"] = cpu_baseline_bwd(w, x, (gq, gk, gv), args.cpu_budget)
     print(json.dumps(res), flush=True)
 
 

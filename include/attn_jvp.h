@@ -135,6 +135,35 @@ int attn_fwd(int dtype, int B, int H, int L, int D,
              const attn_chunk_layout* layout, float softmax_scale,
              void* O, float* LSE, void* stream);
 
+/* Gradient of masked attention (reverse mode): the vector-Jacobian product of the
+ * masked-attention equation (paper App. B) for a cotangent gO of O, as the student's
+ * packed teacher-forcing forward needs for training (Sec. 3.1.2, TF-sCM objective).
+ * With P = exp(s Q K^T - LSE) on admissible pairs and 0 elsewhere:
+ *   Delta = rowsum(gO o O),  gS = P o (gO V^T - Delta),
+ *   gQ = s gS K,  gK = s gS^T Q,  gV = P^T gO.
+ *   in : Q, K, V, O, gO        device [B, H, L, D], dtype `dtype` (O as returned by
+ *                              attn_fwd / attn_jvp_fwd for the same inputs)
+ *        LSE                   device fp32 [B, H, L] from the same call
+ *   out: gQ, gK, gV            device [B, H, L, D], dtype `dtype`
+ *        Delta                 device fp32 [B, H, L]: rowsum(gO o O) (written by the
+ *                              first of the two kernels, read by the second)
+ * Same conventions and error behaviour as attn_jvp_fwd.  The key-side pass needs the
+ * mask transposed into key groups with at most two query ranges each and at most
+ * ATTN_MAX_GROUPS of them: always so for the full, block-causal and teacher-forcing
+ * layouts; an ATTN_MASK_RANGES layout for which it is not so is ATTN_ERR_UNSUPPORTED.
+ * Deterministic (no atomics): two launches on `stream`. */
+int attn_bwd(int dtype, int B, int H, int L, int D,
+             const void* Q, const void* K, const void* V, const void* O, const void* gO,
+             const float* LSE, const attn_chunk_layout* layout, float softmax_scale,
+             void* gQ, void* gK, void* gV, float* Delta, void* stream);
+
+/* Host only.  The mask transposed into key groups, in the layout of
+ * attn_query_groups with keys and queries swapped: 6 int32 per group, k0, k1, a0, a1,
+ * b0, b1 (keys [k0, k1) are admitted by the queries in [a0, a1) and [b0, b1)).
+ * Returns the number of groups, or -1 (ATTN_ERR_UNSUPPORTED message if the transpose
+ * does not fit the two-range form, ATTN_ERR_INVALID for a bad layout or buffer). */
+int attn_key_groups(const attn_chunk_layout* layout, int L, int32_t* out, int max_groups);
+
 /* Host only.  Number of admissible (query, key) pairs of the layout over a
  * sequence of L tokens, i.e. the pairs whose work is counted in throughput
  * figures.  Returns -1 (and sets the error message) for an invalid layout. */

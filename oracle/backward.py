@@ -19,7 +19,9 @@ the reverse-mode derivative of that map: for a cotangent gO of O,
 
 This is that definition written out on whole score rows: no tiling of keys, no
 range lists, no online recurrence.  Query rows are processed in blocks only to
-bound memory.  A row with no admissible key has P = 0 and contributes nothing.
+bound memory, and a block's score rows leave out the keys none of its rows admits
+(their P is exactly zero).  A row with no admissible key has P = 0 and contributes
+nothing.
 """
 import numpy as np
 
@@ -46,22 +48,34 @@ def attention_vjp(Q, K, V, gO, kind, offsets=None, scale=None, rows=None, keys=N
     want_row[rows] = True
     row_pos = np.full(L, -1, dtype=np.int64)
     row_pos[rows] = np.arange(rows.size)
-    # gK, gV need every query row; gQ and Delta only the requested ones
-    visit = np.arange(L) if keys.size else rows
+    # gQ and Delta need the requested rows; gK and gV every row that admits a requested
+    # key (the other rows contribute exactly zero to them)
+    visit_mask = want_row.copy()
+    if keys.size:
+        visit_mask |= allowed_mask(kind, offsets, L, cols=keys).any(axis=1)
+    visit = np.flatnonzero(visit_mask)
     gQ = np.zeros((B, H, rows.size, D))
     Delta = np.zeros((B, H, rows.size))
     gK = np.zeros((B, H, keys.size, D))
     gV = np.zeros((B, H, keys.size, D))
+    key_mask = np.zeros(L, dtype=bool)
+    key_mask[keys] = True
+    key_pos = np.full(L, -1, dtype=np.int64)
+    key_pos[keys] = np.arange(keys.size)
     for r0 in range(0, visit.size, block):
         sel = visit[r0:r0 + block]
         allowed = allowed_mask(kind, offsets, L, sel)
+        # columns no row of the block admits hold P = 0 and are left out (exact zeros)
+        cols = np.flatnonzero(allowed.any(axis=0))
+        a = allowed[:, cols]
+        kc = cols[key_mask[cols]]  # requested keys among them
         for b in range(B):
             for h in range(H):
-                q, k, v, g = Q[b, h, sel], K[b, h], V[b, h], gO[b, h, sel]
-                S = np.where(allowed, s * (q @ k.T), -np.inf)
-                m = S.max(axis=1)
+                q, k, v, g = Q[b, h, sel], K[b, h, cols], V[b, h, cols], gO[b, h, sel]
+                S = np.where(a, s * (q @ k.T), -np.inf)
+                m = S.max(axis=1) if cols.size else np.full(sel.size, -np.inf)
                 empty = ~np.isfinite(m)
-                E = np.where(allowed, np.exp(S - np.where(empty, 0.0, m)[:, None]), 0.0)
+                E = np.where(a, np.exp(S - np.where(empty, 0.0, m)[:, None]), 0.0)
                 l = E.sum(axis=1)
                 P = E / np.where(empty, 1.0, l)[:, None]
                 O = P @ v
@@ -72,7 +86,8 @@ def attention_vjp(Q, K, V, gO, kind, offsets=None, scale=None, rows=None, keys=N
                     pos = row_pos[sel[mine]]
                     gQ[b, h, pos] = s * (gS[mine] @ k)
                     Delta[b, h, pos] = delta[mine]
-                if keys.size:
-                    gK[b, h] += s * (gS[:, keys].T @ q)
-                    gV[b, h] += P[:, keys].T @ g
+                if kc.size:
+                    j = np.searchsorted(cols, kc)
+                    gK[b, h, key_pos[kc]] += s * (gS[:, j].T @ q)
+                    gV[b, h, key_pos[kc]] += P[:, j].T @ g
     return gQ, gK, gV, Delta

@@ -45,22 +45,21 @@ def expected_length(kind, offsets):
     return 2 * half if kind == MASK_TEACHER_FORCING else half
 
 
-def allowed_mask(kind, offsets, L, rows=None):
-    """Boolean matrix allowed[a, b] for query rows ``rows`` (default all) and all L keys."""
+def allowed_mask(kind, offsets, L, rows=None, cols=None):
+    """Boolean matrix allowed[a, b] for query rows ``rows`` and keys ``cols`` (default all)."""
     rows = np.arange(L, dtype=np.int64) if rows is None else np.asarray(rows, dtype=np.int64)
-    cols = np.arange(L, dtype=np.int64)
+    cols = np.arange(L, dtype=np.int64) if cols is None else np.asarray(cols, dtype=np.int64)
     if kind == MASK_FULL:
-        return np.ones((rows.size, L), dtype=bool)
+        return np.ones((rows.size, cols.size), dtype=bool)
     if kind == MASK_RANGES:
         groups = [tuple(int(v) for v in g) for g in offsets]
         assert groups[-1][0] == L, "query groups must cover the sequence"
         q_end = np.array([g[0] for g in groups])
         g_of_row = np.searchsorted(q_end, rows, side="right")
-        out = np.zeros((rows.size, L), dtype=bool)
+        out = np.zeros((rows.size, cols.size), dtype=bool)
         for i, g in enumerate(g_of_row):
             _, a0, a1, b0, b1 = groups[g]
-            out[i, a0:a1] = True
-            out[i, b0:b1] = True
+            out[i] = ((cols >= a0) & (cols < a1)) | ((cols >= b0) & (cols < b1))
         return out
     if kind == MASK_BLOCK_CAUSAL:
         assert L == int(offsets[-1]), "block-causal layout must cover the sequence"

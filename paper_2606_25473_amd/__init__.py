@@ -5,8 +5,8 @@ kernels); :mod:`paper_2606_25473_amd.binding` marshals torch tensors into it.
 Importing this package does not load the library; the first call does, and it
 raises if the library is missing or was built for another target.
 """
-from .binding import (attn_jvp_fwd, attn_jvp_fwd_zero_clean, attn_fwd, count_unmasked_pairs, count_computed_pairs, query_groups,
+from .binding import (attn_jvp_fwd, attn_jvp_fwd_zero_clean, attn_fwd, attn_bwd, count_unmasked_pairs, count_computed_pairs, query_groups,
                       library_path, load_library, AttnError)
 
-__all__ = ["attn_jvp_fwd", "attn_jvp_fwd_zero_clean", "attn_fwd", "count_unmasked_pairs", "count_computed_pairs", "query_groups",
+__all__ = ["attn_jvp_fwd", "attn_jvp_fwd_zero_clean", "attn_fwd", "attn_bwd", "count_unmasked_pairs", "count_computed_pairs", "query_groups",
            "library_path", "load_library", "AttnError"]

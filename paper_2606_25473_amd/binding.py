@@ -57,6 +57,11 @@ def load_library():
     lib.attn_fwd.argtypes = [_i, _i, _i, _i, _i, _vp, _vp, _vp,
                              ctypes.POINTER(_Layout), ctypes.c_float, _vp, _vp, _vp]
     lib.attn_fwd.restype = _i
+    lib.attn_bwd.argtypes = [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp,
+                             ctypes.POINTER(_Layout), ctypes.c_float, _vp, _vp, _vp, _vp, _vp]
+    lib.attn_bwd.restype = _i
+    lib.attn_key_groups.argtypes = [ctypes.POINTER(_Layout), _i, ctypes.POINTER(ctypes.c_int32), _i]
+    lib.attn_key_groups.restype = _i
     lib.attn_count_unmasked_pairs.argtypes = [ctypes.POINTER(_Layout), _i]
     lib.attn_count_unmasked_pairs.restype = ctypes.c_int64
     lib.attn_count_computed_pairs.argtypes = [ctypes.POINTER(_Layout), _i, _i]
@@ -204,6 +209,43 @@ def attn_fwd(q, k, v, kind="teacher_forcing", offsets=None, scale=None, out=None
                           st.cuda_stream)
     _check(rc)
     return o, lse
+
+
+def attn_bwd(q, k, v, o, go, lse, kind="teacher_forcing", offsets=None, scale=None, out=None, stream=None):
+    """(gQ, gK, gV, Delta): gradients of masked attention for the cotangent ``go`` of ``o``.
+
+    q, k, v, o, go: contiguous [B, H, L, D] GPU tensors of one dtype; lse: fp32 [B, H, L]
+    from the forward call that produced ``o``.  ``out`` may supply (gQ, gK, gV, Delta).
+    """
+    lib = load_library()
+    _check_inputs([q, k, v, o, go])
+    B, H, L, D = q.shape
+    if lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, L) or not lse.is_contiguous() \
+            or lse.device != q.device:
+        raise ValueError("lse must be a contiguous fp32 [B, H, L] tensor on q's device")
+    if out is None:
+        gq, gk, gv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+        delta = torch.empty((B, H, L), device=q.device, dtype=torch.float32)
+    else:
+        gq, gk, gv, delta = out
+    lay = make_layout(kind, offsets)
+    st = stream if stream is not None else torch.cuda.current_stream(q.device)
+    with torch.cuda.device(q.device):
+        rc = lib.attn_bwd(_dtype_code(q), B, H, L, D, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                          go.data_ptr(), lse.data_ptr(), ctypes.byref(lay), float(scale or 0.0), gq.data_ptr(),
+                          gk.data_ptr(), gv.data_ptr(), delta.data_ptr(), st.cuda_stream)
+    _check(rc)
+    return gq, gk, gv, delta
+
+
+def key_groups(kind, offsets, L):
+    """The mask transposed into key groups [(k0, k1, a0, a1, b0, b1), ...] (host-only call)."""
+    cap = 2 * MAX_CHUNKS
+    buf = (ctypes.c_int32 * (6 * cap))()
+    n = load_library().attn_key_groups(ctypes.byref(make_layout(kind, offsets)), int(L), buf, cap)
+    if n < 0:
+        raise AttnError(1, last_error())
+    return [tuple(buf[6 * g:6 * g + 6]) for g in range(n)]
 
 
 def count_unmasked_pairs(kind, offsets, L):

@@ -1,0 +1,604 @@
+// attn_bwd.hip -- gradient of masked softmax attention (reverse mode) on gfx950.
+//
+// For a cotangent gO of O = softmax(s Q K^T + M) V (the paper's masked-attention
+// equation, App. B), with P recomputed from the saved LSE (P = exp(s Q K^T - LSE) on
+// admissible pairs, 0 elsewhere):
+//   Delta = rowsum(gO o O),  gP = gO V^T,  gS = P o (gP - Delta),
+//   gQ = s gS K,  gK = s gS^T Q,  gV = P^T gO.
+// Two passes on one stream, neither with atomics (results are deterministic):
+//  - query-tile pass: a work-group owns 256 query rows (8 waves x 32), computes Delta
+//    for them, then streams the key blocks of its plan (the forward's query-group
+//    plan) and accumulates gQ^T = K^T gS^T;
+//  - key-tile pass: a work-group owns 128 keys (4 waves x 32) and two halves of each
+//    64-row query block (waves 0..3 the first 32 rows, 4..7 the second), streams the
+//    query blocks that see its keys (the plan of the transposed, key-group table) and
+//    accumulates gV^T = gO^T P and gK^T = Q^T gS; the two halves are summed at the end.
+// Matrix-core work: 6 D flop per (query, key) pair in the first pass, 8 D in the second
+// (the scores S and gP are computed in both), against 10 D for a single pass that would
+// need atomic gQ updates.
+//
+// fp32 exact-path kernels (one wave per query row, then one wave per key) implement the
+// same two passes for the fp32 entry point.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include "kernels.hpp"
+#include "mfma_common.hpp"
+
+namespace attn {
+namespace {
+
+using namespace dev;
+
+constexpr int NW = 8;  // waves per work-group in both bf16 passes
+constexpr int NTHREADS = 64 * NW;
+
+// ---------------------------------------------------------------- bf16, query-tile pass
+
+constexpr int QBR = kMfmaBr;  // 256 query rows per work-group
+constexpr int QBC = kMfmaBc;  // 32 keys per block
+
+template <int D>
+struct QGeo {
+  static constexpr int ROWB = D * 2;            // bytes per LDS row (bf16)
+  static constexpr int TILEB = QBC * ROWB;      // one K or V tile of a key block
+  static constexpr int DT = D / 32;             // 32-wide d tiles of gQ^T
+  static constexpr int KS = D / 16;             // 16-deep k steps over d
+  static constexpr int IPT = TILEB / 1024;      // 1 KiB direct loads per tile
+};
+
+// Per-lane offsets of the transposed operand reads (ds_read_b64_tr_b16) of a 32-row
+// tile whose rows are listed in the accumulator order of a 32x32 MFMA output:
+// tro[t][p][dt] for k step t (16 rows), row half p (+0 / +8), d tile dt.  In each
+// 16-lane group, lane j receives element j%4 of the 8-byte word addressed by lane
+// 4e + j/4 (e = result element); the addresses below make the row order of the
+// operand equal to that of the B operand taken from the lane's own accumulator.
+template <int D>
+__device__ __forceinline__ void tr_offsets(int lane, int tro[2][2][D / 32]) {
+  const int g16 = lane >> 4, s16 = lane & 15;
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt) {
+        const int r = 16 * t + 8 * p + 4 * (g16 >> 1) + (s16 >> 2);
+        const int chunk = 4 * dt + 2 * (g16 & 1) + ((s16 & 3) >> 1);
+        tro[t][p][dt] = lds_off<D>(r, chunk) + 8 * (s16 & 1);
+      }
+}
+
+template <int D>
+__global__ __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_bwd_dq_kernel(const BwdArgs a) {
+  using G = QGeo<D>;
+  constexpr int TB = G::TILEB;
+  constexpr int SB = 2 * TB;  // stage: K and V tiles of one key block
+  __shared__ __attribute__((aligned(1024))) char stages[3 * SB];
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const int hh = lane >> 5;
+  const int L = a.L;
+
+  const int nqt = a.order.nt;
+  const int bh = blockIdx.x / nqt;
+  const int qtile = tile_of(a.order, blockIdx.x - bh * nqt);
+  const size_t head = (size_t)bh * L * D;
+  const bf16_t* __restrict__ Qg = (const bf16_t*)a.Q + head;
+  const bf16_t* __restrict__ Kg = (const bf16_t*)a.K + head;
+  const bf16_t* __restrict__ Vg = (const bf16_t*)a.V + head;
+  const bf16_t* __restrict__ Og = (const bf16_t*)a.O + head;
+  const bf16_t* __restrict__ gOg = (const bf16_t*)a.gO + head;
+
+  const int q0 = qtile * QBR;
+  const int q1 = q0 + QBR < L ? q0 + QBR : L;
+  const TilePlan plan = plan_tile(a.gt, q0, q1, QBC);
+  const int nblk = plan_num_blocks(plan);
+
+  const int qrow = wave * 32 + (lane & 31);
+  const int row = q0 + qrow;
+  int ra0 = 0, ra1 = 0, rb0 = 0, rb1 = 0;
+  for (int g = plan.g_first; g <= plan.g_last; ++g) {
+    if (row >= group_q_begin(a.gt, g) && row < a.gt.q_end[g]) {
+      ra0 = a.gt.a0[g]; ra1 = a.gt.a1[g]; rb0 = a.gt.b0[g]; rb1 = a.gt.b1[g];
+    }
+  }
+
+  // Q^T and gO^T as B operands in registers (lane: row l%32, d = 16 s + 8 (l/32) + 0..7);
+  // rows past the end are clamped to the last row (their results are not stored)
+  const size_t rbase = (size_t)min(row, L - 1) * D;
+  bf16x8 qop[G::KS], gop[G::KS];
+  float dpart = 0.f;
+#pragma unroll
+  for (int s = 0; s < G::KS; ++s) {
+    qop[s] = *(const bf16x8*)(Qg + rbase + 16 * s + 8 * hh);
+    gop[s] = *(const bf16x8*)(gOg + rbase + 16 * s + 8 * hh);
+    const bf16x8 ov = *(const bf16x8*)(Og + rbase + 16 * s + 8 * hh);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) dpart = fmaf((float)gop[s][j], (float)ov[j], dpart);
+  }
+  // Delta of this row: the two half-waves hold complementary halves of d
+  const float delta = dpart + xor32(dpart);
+  const float lse = a.LSE[(size_t)bh * L + min(row, L - 1)];
+  // a row without admissible keys has LSE = -inf; all its pairs are masked below
+  const float lse2 = lse == -INFINITY ? 0.f : lse * kLog2e;
+  if (row < L && hh == 0) a.Delta[(size_t)bh * L + row] = delta;
+
+  constexpr int RPI = 1024 / G::ROWB;
+  const int dma_r = (lane * 16) / G::ROWB;
+  const int dma_phys = ((lane * 16) % G::ROWB) >> 4;
+  auto dma_tile = [&](const bf16_t* src, int k0, unsigned dst) {
+#pragma unroll
+    for (int j0 = 0; j0 < G::IPT; j0 += NW) {
+      const int j = j0 + wave;
+      if (G::IPT % NW == 0 || j < G::IPT) {
+        const int rr = j * RPI + dma_r;
+        const unsigned grow = (unsigned)min(k0 + rr, L - 1);
+        const unsigned off = (grow * D + (unsigned)((dma_phys ^ swz<D>(rr)) * 8)) * 2u;
+        lds_load16(src, off, dst + (unsigned)(j * RPI * G::ROWB));
+      }
+    }
+  };
+  auto dma_block = [&](int kb, unsigned st) {
+    dma_tile(Kg, kb * QBC, st);
+    dma_tile(Vg, kb * QBC, st + TB);
+  };
+
+  int tro[2][2][G::DT];
+  tr_offsets<D>(lane, tro);
+
+  f32x16 gacc[G::DT];
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt) gacc[dt] = f32x16{};
+  const float c2 = a.scale * kLog2e;
+  const int krow = lane & 31;
+
+  // wait for every load but this iteration's prefetch (2 per wave at D = 128; at D = 64
+  // waves 0..3 issue one per tile and the others none), then synchronise
+  auto end_iteration = []() { asm volatile("s_waitcnt vmcnt(2) lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+  static_assert((G::IPT + NW - 1) / NW == 1, "one direct load per tile and wave");
+
+  auto step = [&](int it, const char* cK, const char* cV, unsigned next_stage) {
+    dma_block(plan_block(plan, min(it + 2, nblk - 1)), next_stage);
+    const int k0 = plan_block(plan, it) * QBC;
+    // S^T = K Q^T and gP^T = V gO^T (lane: query l%32, keys 8 (i/4) + 4 (l/32) + i%4)
+    f32x16 S = f32x16{}, GP = f32x16{};
+#pragma unroll
+    for (int s = 0; s < G::KS; ++s) {
+      const int off = lds_off<D>(krow, 2 * s + hh);
+      S = mfma(*(const bf16x8*)(cK + off), qop[s], S);
+      GP = mfma(*(const bf16x8*)(cV + off), gop[s], GP);
+    }
+    // P^T = exp(S^T - LSE) on admissible pairs, gS^T = P^T o (gP^T - Delta)
+    float gs[16];
+    const bool full = block_is_full(plan, k0, QBC, L);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      float p = __builtin_amdgcn_exp2f(fmaf(S[i], c2, -lse2));
+      if (!full) {
+        const int key = k0 + 8 * (i >> 2) + 4 * hh + (i & 3);
+        const bool ok = (unsigned)(key - ra0) < (unsigned)(ra1 - ra0) ||
+                        (unsigned)(key - rb0) < (unsigned)(rb1 - rb0);
+        p = ok ? p : 0.f;
+      }
+      gs[i] = p * (GP[i] - delta);
+    }
+    // gQ^T += K^T gS^T (K^T from transposed LDS reads, gS^T from this lane's registers)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      bf16x8 gsb;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) gsb[j] = (bf16_t)gs[8 * t + j];
+#pragma unroll
+      for (int dt = 0; dt < G::DT; ++dt) {
+        const bf16x8 kt = cat(ld_tr(cK + tro[t][0][dt]), ld_tr(cK + tro[t][1][dt]));
+        gacc[dt] = mfma(kt, gsb, gacc[dt]);
+      }
+    }
+    end_iteration();
+  };
+
+  const unsigned st_lds = __builtin_amdgcn_readfirstlane(lds_addr(stages));
+  if (nblk > 0) {
+    dma_block(plan_block(plan, 0), st_lds);
+    dma_block(plan_block(plan, min(1, nblk - 1)), st_lds + SB);
+  }
+  __builtin_amdgcn_s_waitcnt(0xF70);  // (builtin: also retires the operand loads above)
+  __syncthreads();
+  int cur = 0;
+  for (int it = 0; it < nblk; ++it) {
+    const int nxt = cur == 0 ? 2 : cur - 1;  // (it + 2) mod 3
+    const char* cs = stages + cur * SB;
+    step(it, cs, cs + TB, st_lds + (unsigned)(nxt * SB));
+    cur = cur == 2 ? 0 : cur + 1;
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the clamped tail prefetches
+
+  if (row < L) {
+    bf16_t* gQg = (bf16_t*)a.gQ + head + (size_t)row * D;
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        bf16x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = (bf16_t)(a.scale * gacc[dt][4 * q4 + e]);
+        *(bf16x4*)(gQg + 32 * dt + 8 * q4 + 4 * hh) = v;
+      }
+  }
+}
+
+// ---------------------------------------------------------------- bf16, key-tile pass
+
+constexpr int KT = kBwdKeysPerTile;   // 128 keys per work-group (4 key groups of 32)
+
+template <int N>
+struct IC {  // a compile-time count passed to a generic lambda
+  static constexpr int value = N;
+};
+constexpr int QB = kBwdRowsPerBlock;  // 64 query rows per block (2 halves of 32)
+
+// Direct global -> LDS load of 4 bytes per lane (lane l's bytes land at lds + 4 l);
+// same contract as lds_load16.
+__device__ __forceinline__ void lds_load4(const void* gbase, unsigned byte_off, unsigned lds) {
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dword %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(byte_off), "s"(gbase), "s"(__builtin_amdgcn_readfirstlane(lds))
+      : "memory");
+}
+
+template <int D>
+struct KGeo {
+  static constexpr int ROWB = D * 2;
+  static constexpr int KTB = KT * ROWB;         // K (or V) rows of the work-group's keys
+  static constexpr int QTB = QB * ROWB;         // Q (or gO) rows of one query block
+  static constexpr int SB = 2 * QTB + 2 * 4 * QB;  // stage: Q, gO, LSE, Delta of a block
+  static constexpr int BYTES = 2 * KTB + 2 * SB;
+  static constexpr int DT = D / 32;
+  static constexpr int KS = D / 16;
+  static constexpr int IPK = KTB / 1024;        // 1 KiB direct loads per key tile
+  static constexpr int IPQ = QTB / 1024;        // ... per query block tensor
+  static constexpr int NACC = 2 * DT * 16;      // accumulator floats per lane (gK^T, gV^T)
+  static_assert(4 * 64 * NACC * 4 <= BYTES, "the half-sum exchange fits in LDS");
+};
+
+template <int D>
+__global__ __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_bwd_dkdv_kernel(const BwdArgs a) {
+  using G = KGeo<D>;
+  __shared__ __attribute__((aligned(1024))) char lds[G::BYTES];
+  char* const sK = lds;
+  char* const sV = lds + G::KTB;
+  char* const stages = lds + 2 * G::KTB;
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const int hh = lane >> 5;
+  const int kw = wave & 3;   // which 32 keys of the tile
+  const int qh = wave >> 2;  // which 32 rows of each query block
+  const int L = a.L;
+
+  const int nkt = a.order.nt;
+  const int bh = blockIdx.x / nkt;
+  const int ktile = tile_of(a.order, blockIdx.x - bh * nkt);
+  const size_t head = (size_t)bh * L * D;
+  const bf16_t* __restrict__ Qg = (const bf16_t*)a.Q + head;
+  const bf16_t* __restrict__ Kg = (const bf16_t*)a.K + head;
+  const bf16_t* __restrict__ Vg = (const bf16_t*)a.V + head;
+  const bf16_t* __restrict__ gOg = (const bf16_t*)a.gO + head;
+  const float* __restrict__ LSEg = a.LSE + (size_t)bh * L;
+  const float* __restrict__ Dg = a.Delta + (size_t)bh * L;
+
+  // plan over the key-group table: the query blocks that see the tile's keys
+  const int k0 = ktile * KT;
+  const int k1 = k0 + KT < L ? k0 + KT : L;
+  const TilePlan plan = plan_tile(a.gt, k0, k1, QB);
+  const int nblk = plan_num_blocks(plan);
+
+  const int krow = kw * 32 + (lane & 31);  // this lane's key within the tile
+  const int key = k0 + krow;
+  int ra0 = 0, ra1 = 0, rb0 = 0, rb1 = 0;  // query ranges that admit this key
+  for (int g = plan.g_first; g <= plan.g_last; ++g) {
+    if (key >= group_q_begin(a.gt, g) && key < a.gt.q_end[g]) {
+      ra0 = a.gt.a0[g]; ra1 = a.gt.a1[g]; rb0 = a.gt.b0[g]; rb1 = a.gt.b1[g];
+    }
+  }
+
+  constexpr int RPI = 1024 / G::ROWB;
+  const int dma_r = (lane * 16) / G::ROWB;
+  const int dma_phys = ((lane * 16) % G::ROWB) >> 4;
+  // n_instr 1 KiB loads of rows [row0, ...) of src into dst, instruction j by wave j % NW
+  auto dma_rows = [&](const bf16_t* src, int row0, unsigned dst, auto n_instr) {
+    constexpr int N = decltype(n_instr)::value;
+#pragma unroll
+    for (int j0 = 0; j0 < N; j0 += NW) {
+      const int j = j0 + wave;
+      if (N % NW == 0 || j < N) {
+        const int rr = j * RPI + dma_r;
+        const unsigned grow = (unsigned)min(row0 + rr, L - 1);
+        const unsigned off = (grow * D + (unsigned)((dma_phys ^ swz<D>(rr)) * 8)) * 2u;
+        lds_load16(src, off, dst + (unsigned)(j * RPI * G::ROWB));
+      }
+    }
+  };
+  // query block qb into the stage at LDS address st: Q and gO rows, LSE and Delta values
+  auto dma_qblock = [&](int qb, unsigned st) {
+    const int r0 = qb * QB;
+    dma_rows(Qg, r0, st, IC<G::IPQ>{});
+    dma_rows(gOg, r0, st + G::QTB, IC<G::IPQ>{});
+    const unsigned roff = (unsigned)min(r0 + lane, L - 1) * 4u;
+    if (wave == NW - 2) lds_load4(LSEg, roff, st + 2 * G::QTB);
+    if (wave == NW - 1) lds_load4(Dg, roff, st + 2 * G::QTB + 4 * QB);
+  };
+
+  int tro[2][2][G::DT];
+  tr_offsets<D>(lane, tro);
+  const int qoff = qh * 32 * G::ROWB;  // this wave's 32 rows within a query block tile
+
+  f32x16 gk[G::DT], gv[G::DT];
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt) {
+    gk[dt] = f32x16{};
+    gv[dt] = f32x16{};
+  }
+  const float c2 = a.scale * kLog2e;
+
+  const unsigned lds_base = __builtin_amdgcn_readfirstlane(lds_addr(lds));
+  const unsigned st_lds = lds_base + 2 * G::KTB;
+  dma_rows(Kg, k0, lds_base, IC<G::IPK>{});
+  dma_rows(Vg, k0, lds_base + G::KTB, IC<G::IPK>{});
+  if (nblk > 0) dma_qblock(plan_block(plan, 0), st_lds);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+
+  for (int it = 0; it < nblk; ++it) {
+    const char* cs = stages + (it & 1) * G::SB;
+    // the other stage was last read in iteration it-1, before the barrier that ended it
+    if (it + 1 < nblk) dma_qblock(plan_block(plan, it + 1), st_lds + (unsigned)(((it + 1) & 1) * G::SB));
+    const int q0b = plan_block(plan, it) * QB;
+
+    // S = Q K^T and gP = gO V^T (lane: key l%32, rows 8 (i/4) + 4 (l/32) + i%4 of the half)
+    f32x16 S = f32x16{}, GP = f32x16{};
+#pragma unroll
+    for (int s = 0; s < G::KS; ++s) {
+      const int aoff = qoff + lds_off<D>(lane & 31, 2 * s + hh);
+      const int boff = lds_off<D>(krow, 2 * s + hh);
+      S = mfma(*(const bf16x8*)(cs + aoff), *(const bf16x8*)(sK + boff), S);
+      GP = mfma(*(const bf16x8*)(cs + G::QTB + aoff), *(const bf16x8*)(sV + boff), GP);
+    }
+    // LSE and Delta of the lane's 16 rows (4 runs of 4 consecutive rows)
+    const float* sl = (const float*)(cs + 2 * G::QTB);
+    const float* sd = sl + QB;
+    float p[16], gs[16];
+    const bool full = block_is_full(plan, q0b, QB, L);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int r = 32 * qh + 8 * c + 4 * hh;
+      const float4 lv = *(const float4*)(sl + r);
+      const float4 dv = *(const float4*)(sd + r);
+      const float lsev[4] = {lv.x, lv.y, lv.z, lv.w};
+      const float dlv[4] = {dv.x, dv.y, dv.z, dv.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int i = 4 * c + e;
+        // rows without admissible keys (LSE = -inf) are masked for every key
+        const float l2 = lsev[e] == -INFINITY ? 0.f : lsev[e] * kLog2e;
+        float pv = __builtin_amdgcn_exp2f(fmaf(S[i], c2, -l2));
+        if (!full) {
+          const int q = q0b + r + e;
+          const bool ok = (unsigned)(q - ra0) < (unsigned)(ra1 - ra0) ||
+                          (unsigned)(q - rb0) < (unsigned)(rb1 - rb0);
+          pv = ok ? pv : 0.f;
+        }
+        p[i] = pv;
+        gs[i] = pv * (GP[i] - dlv[e]);
+      }
+    }
+    // gV^T += gO^T P and gK^T += Q^T gS (transposed LDS reads of the block's rows)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      bf16x8 pb, gsb;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        pb[j] = (bf16_t)p[8 * t + j];
+        gsb[j] = (bf16_t)gs[8 * t + j];
+      }
+#pragma unroll
+      for (int dt = 0; dt < G::DT; ++dt) {
+        const char* qs = cs + qoff;
+        const bf16x8 got = cat(ld_tr(qs + G::QTB + tro[t][0][dt]), ld_tr(qs + G::QTB + tro[t][1][dt]));
+        gv[dt] = mfma(got, pb, gv[dt]);
+        const bf16x8 qt = cat(ld_tr(qs + tro[t][0][dt]), ld_tr(qs + tro[t][1][dt]));
+        gk[dt] = mfma(qt, gsb, gk[dt]);
+      }
+    }
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  }
+
+  // Sum the two row halves: waves 4..7 leave their partial gK^T, gV^T in LDS (every
+  // stage is idle after the last barrier), waves 0..3 add them and store.
+  float* red = (float*)lds + (size_t)kw * G::NACC * 64 + lane;
+  if (qh == 1) {
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        red[(dt * 16 + i) * 64] = gk[dt][i];
+        red[((G::DT + dt) * 16 + i) * 64] = gv[dt][i];
+      }
+  }
+  __syncthreads();
+  if (qh == 0 && key < L) {
+    bf16_t* gKg = (bf16_t*)a.gK + head + (size_t)key * D;
+    bf16_t* gVg = (bf16_t*)a.gV + head + (size_t)key * D;
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        bf16x4 kv, vv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int i = 4 * q4 + e;
+          kv[e] = (bf16_t)(a.scale * (gk[dt][i] + red[(dt * 16 + i) * 64]));
+          vv[e] = (bf16_t)(gv[dt][i] + red[((G::DT + dt) * 16 + i) * 64]);
+        }
+        const int d = 32 * dt + 8 * q4 + 4 * hh;
+        *(bf16x4*)(gKg + d) = kv;
+        *(bf16x4*)(gVg + d) = vv;
+      }
+  }
+}
+
+// ---------------------------------------------------------------- fp32 exact path
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+// One wave per query row: Delta and gQ over the row's key ranges, key by key.
+template <int D>
+__global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_bwd_simt_dq_kernel(const BwdArgs a) {
+  constexpr int E = D / 64;
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * kSimtRowsPerBlock + (threadIdx.x >> 6);
+  const int bh = blockIdx.y;
+  const int L = a.L;
+  if (row >= L) return;
+  const size_t head = (size_t)bh * L * D;
+  const float* Q = (const float*)a.Q + head;
+  const float* K = (const float*)a.K + head;
+  const float* V = (const float*)a.V + head;
+  const float* O = (const float*)a.O + head;
+  const float* gO = (const float*)a.gO + head;
+  const int g = find_group(a.gt, row);
+  const int rng[2][2] = {{a.gt.a0[g], a.gt.a1[g]}, {a.gt.b0[g], a.gt.b1[g]}};
+  float q[E], go[E], acc[E];
+  float dp = 0.f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const size_t i = (size_t)row * D + lane + 64 * e;
+    q[e] = Q[i];
+    go[e] = gO[i];
+    acc[e] = 0.f;
+    dp += go[e] * O[i];
+  }
+  const float delta = wave_sum(dp);
+  const float lse = a.LSE[(size_t)bh * L + row];
+  const float sc = a.scale;
+  for (int ri = 0; ri < 2; ++ri) {
+    for (int k = rng[ri][0]; k < rng[ri][1]; ++k) {
+      float s = 0.f, gp = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        s += q[e] * K[(size_t)k * D + lane + 64 * e];
+        gp += go[e] * V[(size_t)k * D + lane + 64 * e];
+      }
+      s = wave_sum(s) * sc;
+      gp = wave_sum(gp);
+      const float gs = expf(s - lse) * (gp - delta);
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e] += gs * K[(size_t)k * D + lane + 64 * e];
+    }
+  }
+  float* gQ = (float*)a.gQ + head + (size_t)row * D;
+#pragma unroll
+  for (int e = 0; e < E; ++e) gQ[lane + 64 * e] = sc * acc[e];
+  if (lane == 0) a.Delta[(size_t)bh * L + row] = delta;
+}
+
+// One wave per key: gK and gV over the query ranges that admit the key.
+template <int D>
+__global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_bwd_simt_dkdv_kernel(const BwdArgs a) {
+  constexpr int E = D / 64;
+  const int lane = threadIdx.x & 63;
+  const int key = blockIdx.x * kSimtRowsPerBlock + (threadIdx.x >> 6);
+  const int bh = blockIdx.y;
+  const int L = a.L;
+  if (key >= L) return;
+  const size_t head = (size_t)bh * L * D;
+  const float* Q = (const float*)a.Q + head;
+  const float* K = (const float*)a.K + head;
+  const float* V = (const float*)a.V + head;
+  const float* gO = (const float*)a.gO + head;
+  const float* LSE = a.LSE + (size_t)bh * L;
+  const float* Dl = a.Delta + (size_t)bh * L;
+  const int g = find_group(a.gt, key);  // key-group table
+  const int rng[2][2] = {{a.gt.a0[g], a.gt.a1[g]}, {a.gt.b0[g], a.gt.b1[g]}};
+  float k[E], v[E], gk[E], gv[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    k[e] = K[(size_t)key * D + lane + 64 * e];
+    v[e] = V[(size_t)key * D + lane + 64 * e];
+    gk[e] = 0.f;
+    gv[e] = 0.f;
+  }
+  const float sc = a.scale;
+  for (int ri = 0; ri < 2; ++ri) {
+    for (int q = rng[ri][0]; q < rng[ri][1]; ++q) {
+      float s = 0.f, gp = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        s += Q[(size_t)q * D + lane + 64 * e] * k[e];
+        gp += gO[(size_t)q * D + lane + 64 * e] * v[e];
+      }
+      s = wave_sum(s) * sc;
+      gp = wave_sum(gp);
+      const float p = expf(s - LSE[q]);
+      const float gs = p * (gp - Dl[q]);
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        gk[e] += gs * Q[(size_t)q * D + lane + 64 * e];
+        gv[e] += p * gO[(size_t)q * D + lane + 64 * e];
+      }
+    }
+  }
+  float* gK = (float*)a.gK + head + (size_t)key * D;
+  float* gV = (float*)a.gV + head + (size_t)key * D;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    gK[lane + 64 * e] = sc * gk[e];
+    gV[lane + 64 * e] = gv[e];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_bwd_mfma_bf16(const BwdArgs& qa, const BwdArgs& ka, int D, hipStream_t stream) {
+  const dim3 gq((unsigned)(qa.order.nt * qa.B * qa.H)), gk((unsigned)(ka.order.nt * ka.B * ka.H));
+  const dim3 block(NTHREADS);
+  if (D == 128) {
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<128>), gq, block, 0, stream, qa);
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<128>), gk, block, 0, stream, ka);
+  } else {
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<64>), gq, block, 0, stream, qa);
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<64>), gk, block, 0, stream, ka);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_simt_f32(const BwdArgs& qa, const BwdArgs& ka, int D, hipStream_t stream) {
+  const dim3 grid((unsigned)((qa.L + kSimtRowsPerBlock - 1) / kSimtRowsPerBlock), (unsigned)(qa.B * qa.H));
+  const dim3 block(64 * kSimtRowsPerBlock);
+  if (D == 128) {
+    hipLaunchKernelGGL((attn_bwd_simt_dq_kernel<128>), grid, block, 0, stream, qa);
+    hipLaunchKernelGGL((attn_bwd_simt_dkdv_kernel<128>), grid, block, 0, stream, ka);
+  } else {
+    hipLaunchKernelGGL((attn_bwd_simt_dq_kernel<64>), grid, block, 0, stream, qa);
+    hipLaunchKernelGGL((attn_bwd_simt_dkdv_kernel<64>), grid, block, 0, stream, ka);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace attn

@@ -102,6 +102,67 @@ int launch(attn::Pass pass, int dtype, int D, const attn::AttnArgs& args, void* 
   return ATTN_OK;
 }
 
+int prepare_bwd(int dtype, int B, int H, int L, int D, const void* Q, const void* K, const void* V,
+                const void* O, const void* gO, const float* LSE, const attn_chunk_layout* layout,
+                float softmax_scale, void* gQ, void* gK, void* gV, float* Delta, attn::BwdArgs* qa,
+                attn::BwdArgs* ka) {
+  if (dtype != ATTN_DTYPE_F32 && dtype != ATTN_DTYPE_BF16)
+    return fail(ATTN_ERR_UNSUPPORTED, "unsupported dtype " + std::to_string(dtype));
+  if (D != 64 && D != 128)
+    return fail(ATTN_ERR_UNSUPPORTED, "unsupported head_dim " + std::to_string(D) + " (built: 64, 128)");
+  if (B <= 0 || H <= 0 || L <= 0)
+    return fail(ATTN_ERR_INVALID, "B, H and L must be positive (B=" + std::to_string(B) +
+                                      ", H=" + std::to_string(H) + ", L=" + std::to_string(L) + ")");
+  if ((int64_t)B * H > (int64_t)1 << 20) return fail(ATTN_ERR_INVALID, "B * H too large");
+  const void* ins[6] = {Q, K, V, O, gO, LSE};
+  const char* in_names[6] = {"Q", "K", "V", "O", "gO", "LSE"};
+  void* outs[4] = {gQ, gK, gV, Delta};
+  const char* out_names[4] = {"gQ", "gK", "gV", "Delta"};
+  for (int i = 0; i < 6; ++i)
+    if (!ins[i]) return fail(ATTN_ERR_INVALID, std::string("NULL pointer ") + in_names[i]);
+  for (int i = 0; i < 4; ++i)
+    if (!outs[i]) return fail(ATTN_ERR_INVALID, std::string("NULL pointer ") + out_names[i]);
+  const uintptr_t tbytes = (uintptr_t)B * H * L * D * elem_size(dtype);
+  const uintptr_t lbytes = (uintptr_t)B * H * L * sizeof(float);
+  const uintptr_t align = dtype == ATTN_DTYPE_BF16 ? 16 : 4;
+  for (int i = 0; i < 6; ++i)
+    if ((uintptr_t)ins[i] % (i < 5 ? align : 4))
+      return fail(ATTN_ERR_INVALID, std::string(in_names[i]) + " is misaligned");
+  for (int i = 0; i < 4; ++i)
+    if ((uintptr_t)outs[i] % (i < 3 ? align : 4))
+      return fail(ATTN_ERR_INVALID, std::string(out_names[i]) + " is misaligned");
+  for (int i = 0; i < 4; ++i) {
+    const Span o = {(uintptr_t)outs[i], (uintptr_t)outs[i] + (i < 3 ? tbytes : lbytes), out_names[i]};
+    for (int j = i + 1; j < 4; ++j) {
+      const Span p = {(uintptr_t)outs[j], (uintptr_t)outs[j] + (j < 3 ? tbytes : lbytes), out_names[j]};
+      if (overlap(o, p))
+        return fail(ATTN_ERR_INVALID, std::string("outputs ") + o.name + " and " + p.name + " overlap");
+    }
+    for (int k = 0; k < 6; ++k) {
+      const Span in = {(uintptr_t)ins[k], (uintptr_t)ins[k] + (k < 5 ? tbytes : lbytes), in_names[k]};
+      if (overlap(o, in))
+        return fail(ATTN_ERR_INVALID, std::string("output ") + o.name + " overlaps input " + in.name);
+    }
+  }
+  std::string err;
+  if (!attn::build_groups(layout, L, &qa->gt, &err)) return fail(ATTN_ERR_INVALID, err);
+  if (!attn::transpose_groups(qa->gt, L, &ka->gt, &err)) return fail(ATTN_ERR_UNSUPPORTED, err);
+  qa->Q = ka->Q = Q; qa->K = ka->K = K; qa->V = ka->V = V;
+  qa->O = ka->O = O; qa->gO = ka->gO = gO; qa->LSE = ka->LSE = LSE;
+  qa->gQ = ka->gQ = gQ; qa->gK = ka->gK = gK; qa->gV = ka->gV = gV; qa->Delta = ka->Delta = Delta;
+  qa->B = ka->B = B; qa->H = ka->H = H; qa->L = ka->L = L;
+  qa->scale = ka->scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)D);
+  qa->order = attn::make_tile_order(layout, L, attn::kMfmaBr);
+  // key tiles: for the built-in layouts the work per key tile falls with the key index
+  // (earlier keys are seen by more queries), so the natural order is heaviest first
+  ka->order = attn::TileOrder{};
+  ka->order.mode = 0;
+  ka->order.nt = (L + attn::kBwdKeysPerTile - 1) / attn::kBwdKeysPerTile;
+  ka->order.split = ka->order.nt;
+  ka->order.first = -1;
+  return ATTN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -134,6 +195,35 @@ int attn_fwd(int dtype, int B, int H, int L, int D, const void* Q, const void* K
                          softmax_scale, O, nullptr, LSE, &args);
   if (rc != ATTN_OK) return rc;
   return launch(attn::Pass::kFwd, dtype, D, args, stream);
+}
+
+int attn_bwd(int dtype, int B, int H, int L, int D, const void* Q, const void* K, const void* V, const void* O,
+             const void* gO, const float* LSE, const attn_chunk_layout* layout, float softmax_scale, void* gQ,
+             void* gK, void* gV, float* Delta, void* stream) {
+  attn::BwdArgs qa, ka;
+  const int rc = prepare_bwd(dtype, B, H, L, D, Q, K, V, O, gO, LSE, layout, softmax_scale, gQ, gK, gV, Delta,
+                             &qa, &ka);
+  if (rc != ATTN_OK) return rc;
+  const hipError_t e = dtype == ATTN_DTYPE_BF16 ? attn::launch_bwd_mfma_bf16(qa, ka, D, (hipStream_t)stream)
+                                                : attn::launch_bwd_simt_f32(qa, ka, D, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(ATTN_ERR_HIP, std::string("HIP launch failed: ") + hipGetErrorString(e));
+  return ATTN_OK;
+}
+
+int attn_key_groups(const attn_chunk_layout* layout, int L, int32_t* out, int max_groups) {
+  attn::GroupTable gt, kt;
+  std::string err;
+  if (!attn::build_groups(layout, L, &gt, &err)) return fail(ATTN_ERR_INVALID, err), -1;
+  if (!attn::transpose_groups(gt, L, &kt, &err)) return fail(ATTN_ERR_UNSUPPORTED, err), -1;
+  if (!out || max_groups < kt.n) return fail(ATTN_ERR_INVALID, "output buffer too small"), -1;
+  for (int g = 0; g < kt.n; ++g) {
+    int32_t* r = out + 6 * g;
+    r[0] = attn::group_q_begin(kt, g);
+    r[1] = kt.q_end[g];
+    r[2] = kt.a0[g]; r[3] = kt.a1[g];
+    r[4] = kt.b0[g]; r[5] = kt.b1[g];
+  }
+  return kt.n;
 }
 
 int64_t attn_count_unmasked_pairs(const attn_chunk_layout* layout, int L) {

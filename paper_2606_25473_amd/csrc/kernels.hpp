@@ -26,6 +26,26 @@ struct AttnArgs {
   TileOrder order;
 };
 
+// Arguments of one backward launch (reverse mode: gradients from the cotangent gO).
+// `gt` is the query-group table for the query-tile kernels (gQ, Delta) and the
+// transposed key-group table for the key-tile kernels (gK, gV).
+struct BwdArgs {
+  const void* Q;
+  const void* K;
+  const void* V;
+  const void* O;
+  const void* gO;
+  const float* LSE;
+  void* gQ;
+  void* gK;
+  void* gV;
+  float* Delta;     // rowsum(gO o O): written by the query-tile pass, read by the key-tile pass
+  int B, H, L;
+  float scale;
+  GroupTable gt;
+  TileOrder order;
+};
+
 // bf16 MFMA kernels: query tiles of kMfmaBr rows (8 waves x 32 rows), key blocks of kMfmaBc keys.
 constexpr int kMfmaBr = 256;
 constexpr int kMfmaBc = 32;
@@ -39,5 +59,15 @@ enum class Pass { kFwd, kJvp, kJvpZeroClean };
 
 hipError_t launch_mfma_bf16(const AttnArgs& a, int D, Pass pass, hipStream_t stream);
 hipError_t launch_simt_f32(const AttnArgs& a, int D, Pass pass, hipStream_t stream);
+
+// bf16 backward: key tiles of kBwdKeysPerTile keys, query blocks of kBwdRowsPerBlock rows.
+constexpr int kBwdKeysPerTile = 128;
+constexpr int kBwdRowsPerBlock = 64;
+
+// The backward is two launches on one stream: the query-tile pass (gQ and Delta, with
+// `qa` holding the query-group table) and then the key-tile pass (gK and gV, with `ka`
+// holding the key-group table), which reads Delta.
+hipError_t launch_bwd_mfma_bf16(const BwdArgs& qa, const BwdArgs& ka, int D, hipStream_t stream);
+hipError_t launch_bwd_simt_f32(const BwdArgs& qa, const BwdArgs& ka, int D, hipStream_t stream);
 
 }  // namespace attn

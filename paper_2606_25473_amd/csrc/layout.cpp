@@ -2,8 +2,10 @@
 // table, pair counts and the work-group tile order.  Plain C++17, no HIP.
 #include "layout.hpp"
 
+#include <algorithm>
 #include <cstdio>
 #include <string>
+#include <vector>
 
 namespace attn {
 
@@ -78,6 +80,47 @@ bool build_groups(const attn_chunk_layout* layout, int L, GroupTable* gt, std::s
   for (int j = 0; j < N; ++j) add_group(gt, o[j + 1], 0, o[j + 1], 0, 0);
   // noisy chunk i: clean chunks < i, then its own noisy chunk
   for (int i = 0; i < N; ++i) add_group(gt, half + o[i + 1], 0, o[i], half + o[i], half + o[i + 1]);
+  return true;
+}
+
+bool transpose_groups(const GroupTable& gt, int L, GroupTable* kt, std::string* err) {
+  // key breakpoints: every range end point; between two of them the admitting groups are fixed
+  std::vector<int> cuts = {0, L};
+  for (int g = 0; g < gt.n; ++g) {
+    if (gt.a1[g] > gt.a0[g]) { cuts.push_back(gt.a0[g]); cuts.push_back(gt.a1[g]); }
+    if (gt.b1[g] > gt.b0[g]) { cuts.push_back(gt.b0[g]); cuts.push_back(gt.b1[g]); }
+  }
+  std::sort(cuts.begin(), cuts.end());
+  cuts.erase(std::unique(cuts.begin(), cuts.end()), cuts.end());
+  kt->n = 0;
+  for (size_t c = 0; c + 1 < cuts.size(); ++c) {
+    const int k = cuts[c];  // representative key of [cuts[c], cuts[c+1])
+    int runs[2][2] = {{0, 0}, {0, 0}};
+    int nr = 0;
+    for (int g = 0; g < gt.n; ++g) {
+      const bool hit = (k >= gt.a0[g] && k < gt.a1[g]) || (k >= gt.b0[g] && k < gt.b1[g]);
+      if (!hit) continue;
+      const int q0 = group_q_begin(gt, g), q1 = gt.q_end[g];
+      if (nr > 0 && runs[nr - 1][1] == q0) {
+        runs[nr - 1][1] = q1;  // adjacent query groups form one run
+        continue;
+      }
+      if (nr == 2)
+        return fail(err, "the transposed mask needs more than two query ranges for key " + std::to_string(k));
+      runs[nr][0] = q0; runs[nr][1] = q1;
+      ++nr;
+    }
+    const int e = cuts[c + 1];
+    const int n = kt->n;
+    if (n > 0 && kt->a0[n - 1] == runs[0][0] && kt->a1[n - 1] == runs[0][1] && kt->b0[n - 1] == runs[1][0] &&
+        kt->b1[n - 1] == runs[1][1]) {
+      kt->q_end[n - 1] = e;  // same query ranges as the previous key interval: extend it
+      continue;
+    }
+    if (n == kMaxGroups)
+      return fail(err, "the transposed mask needs more than " + std::to_string(kMaxGroups) + " key groups");
+    add_group(kt, e, runs[0][0], runs[0][1], runs[1][0], runs[1][1]);
+  }
   return true;
 }
 

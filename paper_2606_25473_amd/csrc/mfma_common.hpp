@@ -1,0 +1,77 @@
+// mfma_common.hpp -- device helpers shared by the bf16 matrix-core kernels (gfx950):
+// operand types, the LDS row swizzle, MFMA and transposed-LDS-read wrappers, and the
+// direct global -> LDS load.  Device code only; included by the .hip kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+namespace attn {
+namespace dev {
+
+typedef __bf16 bf16_t;
+typedef bf16_t bf16x8 __attribute__((ext_vector_type(8)));
+typedef bf16_t bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// XOR swizzle of 16-byte chunks within an LDS row: conflict-free both for the
+// 16 consecutive rows of a b128 score-operand read and for the 4-row x 4-chunk
+// footprint of a transposed read.
+template <int D>
+__device__ __forceinline__ int swz(int row) {
+  return (((row & 3) << 2) | ((row >> 2) & 3)) & (D / 8 - 1);  // D / 8 chunks per row
+}
+
+template <int D>
+__device__ __forceinline__ int lds_off(int row, int chunk) {
+  return row * (2 * D) + ((chunk ^ swz<D>(row)) << 4);  // rows of D bf16
+}
+
+__device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x4 ld_tr(const char* p) {
+  i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4*)(p));
+  return __builtin_bit_cast(bf16x4, v);
+}
+
+__device__ __forceinline__ bf16x8 cat(bf16x4 a, bf16x4 b) {
+  return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+
+__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32, 64); }
+
+// Direct global -> LDS load of 16 bytes per lane (global_load_lds_dwordx4): lane l's
+// bytes land at LDS address lds + 16 l.  Issued from inline assembly on purpose: the
+// compiler then does not track these loads, so it never inserts waits for them before
+// LDS reads of other pipeline stages (it cannot tell stages apart when the stage index
+// is a run-time value).  The kernel waits for them itself (vmcnt) before a barrier.
+// M0 carries the LDS base address (one wait state separates its write from the load);
+// M0 is saved and restored around the load because the compiler reserves it.
+__device__ __forceinline__ void lds_load16(const void* gbase, unsigned byte_off, unsigned lds) {
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(byte_off), "s"(gbase), "s"(__builtin_amdgcn_readfirstlane(lds))
+      : "memory");
+}
+
+__device__ __forceinline__ unsigned lds_addr(const void* p) {
+  return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+}  // namespace dev
+}  // namespace attn

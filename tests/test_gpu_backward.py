@@ -1,0 +1,174 @@
+"""GPU parity of the masked-attention backward (attn_bwd) against the fp64 oracle (marked ``gpu``).
+
+O and LSE fed to the kernels come from the oracle's forward (O rounded to the input
+dtype, LSE in fp32), so these tests isolate the backward; one test chains the HIP
+forward into the HIP backward.  Outputs gQ, gK, gV and Delta are compared by relative
+L2 error over every element (<= 1e-2 for bf16, <= 1e-4 for fp32; a reference whose
+norm is below 1e-3 of the cotangent's, as for L = 1 where gQ = gK = 0, is compared
+against that floor) on shapes with
+ragged tails, several key tiles and query blocks, one-token and single chunks, D = 64,
+block-causal, full and explicit range masks (including rows with no key and keys no
+row sees); the full Wan2.1-1.3B chunk-wise workload is checked on sampled rows and
+keys; and two launches must agree bit for bit.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention_fwd, attention_vjp
+from paper_2606_25473_amd import attn_bwd, attn_fwd
+from paper_2606_25473_amd.workloads import (MASK_BLOCK_CAUSAL, MASK_FULL, MASK_RANGES, MASK_TEACHER_FORCING,
+                                            WORKLOADS, custom_workload, make_inputs)
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"bf16": 1e-2, "f32": 1e-4}
+
+
+def _say(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def _rel(x, ref, floor=1e-300):
+    """||x - ref|| / ||ref||, with ||ref|| floored (gradients that vanish exactly, as gQ
+    and gK do for a row with one key, are compared against the cotangent's scale)."""
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    return float(np.linalg.norm(x - ref) / max(np.linalg.norm(ref), floor))
+
+
+def _np(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def _offsets(w):
+    return [tuple(g) for g in w.offsets] if w.kind == MASK_RANGES else (list(w.offsets) if w.offsets else None)
+
+
+def _inputs(w, seed):
+    """Q, K, V, gO (the dV draw of the seeded recipe serves as the cotangent)."""
+    x = make_inputs(w, "cpu", seed)
+    return x["Q"], x["K"], x["V"], x["dV"]
+
+
+def _oracle_fwd(w, q, k, v):
+    O, LSE = attention_fwd(_np(q), _np(k), _np(v), w.kind, _offsets(w))
+    return torch.from_numpy(O).to(q.dtype), torch.from_numpy(LSE).float()
+
+
+SHAPES = [
+    custom_workload("bwd_tiny_tf_f32", 1, 2, 64, "f32", MASK_TEACHER_FORCING, 4, 16),
+    custom_workload("bwd_tf_f32_d128", 1, 2, 128, "f32", MASK_TEACHER_FORCING, 3, 20),
+    custom_workload("bwd_tf_ragged_bf16", 2, 2, 128, "bf16", MASK_TEACHER_FORCING, 3, 100, tangent_std=0.5),
+    custom_workload("bwd_tf_several_tiles_bf16", 1, 3, 128, "bf16", MASK_TEACHER_FORCING, 4, 300, tangent_std=0.5),
+    custom_workload("bwd_tf_one_token_chunks_bf16", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, 64, 1,
+                    tangent_std=0.5),
+    custom_workload("bwd_tf_one_chunk_bf16", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, 1, 300, tangent_std=0.5),
+    custom_workload("bwd_tf_nonuniform_bf16", 1, 2, 128, "bf16", MASK_TEACHER_FORCING,
+                    offsets=[0, 1, 3, 7, 40, 41, 90, 200], tangent_std=0.5),
+    custom_workload("bwd_tf_d64_bf16", 1, 2, 64, "bf16", MASK_TEACHER_FORCING, 4, 50, tangent_std=0.5),
+    custom_workload("bwd_block_causal_bf16", 1, 2, 128, "bf16", MASK_BLOCK_CAUSAL,
+                    offsets=[0, 50, 77, 200, 333], tangent_std=0.5),
+    custom_workload("bwd_full_1000_bf16", 1, 2, 128, "bf16", MASK_FULL, L=1000, tangent_std=0.5),
+    custom_workload("bwd_full_below_one_tile_bf16", 1, 1, 128, "bf16", MASK_FULL, L=7, tangent_std=0.5),
+    custom_workload("bwd_full_single_token_bf16", 1, 1, 128, "bf16", MASK_FULL, L=1, tangent_std=0.5),
+    custom_workload("bwd_full_d64_f32", 1, 2, 64, "f32", MASK_FULL, L=50),
+    # rows 100..149 see no key; keys 450..499 are seen by no row
+    custom_workload("bwd_ranges_bf16", 1, 2, 128, "bf16", MASK_RANGES,
+                    offsets=[(100, 0, 100, 300, 350), (150, 0, 0, 0, 0), (400, 0, 450, 0, 0),
+                             (500, 100, 200, 0, 0)], tangent_std=0.5),
+    custom_workload("bwd_ranges_f32", 1, 1, 64, "f32", MASK_RANGES,
+                    offsets=[(10, 0, 10, 30, 35), (15, 0, 0, 0, 0), (40, 0, 20, 0, 0)]),
+]
+
+
+def _check(w, q, k, v, go, o, lse, label):
+    g = [t.cuda() for t in (q, k, v, o, go)]
+    gq, gk, gv, delta = attn_bwd(*g, lse.cuda(), w.kind, _offsets(w))
+    torch.cuda.synchronize()
+    ref = attention_vjp(_np(q), _np(k), _np(v), _np(go), w.kind, _offsets(w))
+    floor = 1e-3 * float(np.linalg.norm(_np(go)))
+    errs = [_rel(_np(a), b, floor) for a, b in zip((gq, gk, gv, delta), ref)]
+    _say(f"[backward] {w.name} {label} rel-L2 gQ={errs[0]:.3e} gK={errs[1]:.3e} gV={errs[2]:.3e} "
+         f"Delta={errs[3]:.3e}")
+    for t in (gq, gk, gv, delta):
+        assert torch.isfinite(t).all()
+    assert max(errs) <= TOL[w.dtype], errs
+    return gq, gk, gv, delta, ref
+
+
+@pytest.mark.parametrize("w", SHAPES, ids=[w.name for w in SHAPES])
+def test_backward_vs_oracle(w):
+    _say(f"[backward] {w.name} B={w.B} H={w.H} L={w.L} D={w.D} {w.dtype} {w.kind}")
+    q, k, v, go = _inputs(w, 11)
+    o, lse = _oracle_fwd(w, q, k, v)
+    gq, gk, gv, delta, ref = _check(w, q, k, v, go, o, lse, "oracle O/LSE")
+    if w.kind == MASK_RANGES:
+        # fully masked rows and unseen keys get exactly zero
+        m = np.zeros(w.L, dtype=bool)
+        for q0g, q1g, grp in zip([0] + [g[0] for g in w.offsets[:-1]], [g[0] for g in w.offsets], w.offsets):
+            if grp[1] == grp[2] and grp[3] == grp[4]:
+                m[q0g:q1g] = True
+        assert (gq[:, :, torch.from_numpy(np.flatnonzero(m)).cuda()] == 0).all()
+        unseen = np.flatnonzero(~np.abs(ref[2]).sum(axis=(0, 1, 3)).astype(bool))
+        if unseen.size:
+            idx = torch.from_numpy(unseen).cuda()
+            assert (gk[:, :, idx] == 0).all() and (gv[:, :, idx] == 0).all()
+
+
+def test_backward_after_hip_forward():
+    """The HIP forward's O and LSE feed the HIP backward (the training pipeline)."""
+    w = custom_workload("bwd_chain_bf16", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, 4, 300, tangent_std=0.5)
+    _say("[backward] chained after attn_fwd")
+    q, k, v, go = _inputs(w, 12)
+    o, lse = attn_fwd(q.cuda(), k.cuda(), v.cuda(), w.kind, list(w.offsets))
+    torch.cuda.synchronize()
+    _check(w, q, k, v, go, o.cpu(), lse.cpu(), "HIP O/LSE")
+
+
+def test_backward_deterministic():
+    w = custom_workload("bwd_determinism", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, 4, 300, tangent_std=0.5)
+    _say("[backward] run-to-run determinism")
+    q, k, v, go = _inputs(w, 13)
+    o, lse = _oracle_fwd(w, q, k, v)
+    g = [t.cuda() for t in (q, k, v, o, go)] + [lse.cuda()]
+    a = attn_bwd(*g, w.kind, list(w.offsets))
+    b = attn_bwd(*g, w.kind, list(w.offsets))
+    torch.cuda.synchronize()
+    for u, t in zip(a, b):
+        assert torch.equal(u, t)
+
+
+def test_backward_full_size_sampled():
+    """Wan2.1-1.3B chunk-wise TF (B=1, H=12, L=65520, D=128, bf16), HIP forward then
+    backward in the launch configuration the bench times; sampled rows of gQ and Delta
+    and sampled keys of gK, gV against the oracle."""
+    w = WORKLOADS["wan1.3b_chunkwise_tf"]
+    _say(f"[backward] full size {w.name}: generating inputs on the GPU")
+    x = make_inputs(w, "cuda", 0)
+    q, k, v, go = x["Q"], x["K"], x["V"], x["dV"]
+    offs = list(w.offsets)
+    o, lse = attn_fwd(q, k, v, w.kind, offs)
+    gq, gk, gv, delta = attn_bwd(q, k, v, o, go, lse, w.kind, offs)
+    torch.cuda.synchronize()
+    _say("[backward] full size: kernels done, checking sampled rows and keys")
+    for t in (gq, gk, gv, delta):
+        assert torch.isfinite(t).all()
+    half = w.L // 2
+    rng = np.random.default_rng(0)
+    rows = np.unique(np.concatenate([[0, half - 1, half, w.L - 1], rng.integers(0, w.L, 20)]))
+    # keys of the last clean chunk and of the first two noisy chunks: each is seen by few
+    # query rows with few keys, which keeps the oracle's work small (~20 s)
+    pools = [np.arange(offs[-2], half), half + np.arange(offs[0], offs[2])]
+    keys = np.unique(np.concatenate([[offs[-2], half - 1, half]] + [rng.choice(p, 6) for p in pools]))
+    for b, h in ((0, w.H - 1),):
+        sl = [_np(t[b:b + 1, h:h + 1]) for t in (q, k, v, go)]
+        rq, rk, rv, rd = attention_vjp(*sl, w.kind, offs, rows=rows, keys=keys)
+        ri, ki = torch.from_numpy(rows).cuda(), torch.from_numpy(keys).cuda()
+        errs = (_rel(_np(gq[b, h].index_select(0, ri)), rq[0, 0]), _rel(_np(gk[b, h].index_select(0, ki)), rk[0, 0]),
+                _rel(_np(gv[b, h].index_select(0, ki)), rv[0, 0]), _rel(_np(delta[b, h].index_select(0, ri)), rd[0, 0]))
+        _say(f"[backward] full size (b={b}, h={h}) {len(rows)} rows / {len(keys)} keys rel-L2 gQ={errs[0]:.3e} "
+             f"gK={errs[1]:.3e} gV={errs[2]:.3e} Delta={errs[3]:.3e}")
+        assert max(errs) <= TOL["bf16"], errs

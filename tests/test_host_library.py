@@ -98,6 +98,39 @@ def test_query_groups_reproduce_mask(lib, kind, offsets, L):
     assert np.array_equal(m, allowed_mask(kind, offsets, L))
 
 
+@pytest.mark.parametrize("kind,offsets,L", LAYOUTS)
+def test_key_groups_reproduce_transposed_mask(lib, kind, offsets, L):
+    """The key-group table of the backward's key-side pass is the mask transposed."""
+    groups = binding.key_groups(kind, offsets, L)
+    mt = np.zeros((L, L), dtype=bool)   # mt[key, query]
+    prev = 0
+    for k0, k1, a0, a1, b0, b1 in groups:
+        assert k0 == prev and k1 > k0
+        prev = k1
+        assert a0 <= a1 and b0 <= b1 and (a1 <= b0 or b1 == b0)
+        mt[k0:k1, a0:a1] = True
+        mt[k0:k1, b0:b1] = True
+    assert prev == L
+    assert np.array_equal(mt, allowed_mask(kind, offsets, L).T)
+
+
+def test_key_groups_of_teacher_forcing_closed_form(lib):
+    # clean chunk j is seen by the clean queries from chunk j on and the noisy queries
+    # of later chunks; noisy chunk i by its own noisy queries only
+    offs = [0, 3, 7, 10]
+    assert binding.key_groups("teacher_forcing", offs, 20) == [
+        (0, 3, 0, 10, 13, 20), (3, 7, 3, 10, 17, 20), (7, 10, 7, 10, 0, 0),
+        (10, 13, 10, 13, 0, 0), (13, 17, 13, 17, 0, 0), (17, 20, 17, 20, 0, 0)]
+
+
+def test_key_groups_reject_three_query_ranges(lib):
+    # key 0 is admitted by groups 0, 2 and 4, which are not adjacent: three query runs
+    groups = [(2, 0, 1, 0, 0), (4, 1, 2, 0, 0), (6, 0, 1, 0, 0), (8, 1, 2, 0, 0), (10, 0, 1, 0, 0)]
+    with pytest.raises(binding.AttnError):
+        binding.key_groups("ranges", groups, 10)
+    assert "two query ranges" in binding.last_error()
+
+
 @pytest.mark.parametrize("seed", range(6))
 def test_random_range_lists(lib, seed):
     L = int(np.random.default_rng(seed).integers(40, 900))
@@ -258,6 +291,26 @@ def test_zero_clean_entry_point_validates(lib):
                                      ctypes.byref(make_layout("teacher_forcing", [0, 16, 40])), 0.0,
                                      q[6], q[7], q[8], None)
     assert rc == 1 and "L = 2" in binding.last_error()
+
+
+@_no_gpu
+def test_backward_entry_point_validates(lib):
+    # Q, K, V, O, gO, LSE, gQ, gK, gV, Delta as fake bf16 [1, 1, 64, 64] / fp32 [1, 1, 64]
+    p = _ptrs(10)
+
+    def call(ptrs, layout=None, dtype=1, D=64):
+        lay = layout or make_layout("full")
+        return lib.attn_bwd(dtype, 1, 1, 64, D, *ptrs[:6], ctypes.byref(lay), 0.0, *ptrs[6:], None)
+
+    q = list(p); q[4] = 0
+    assert call(q) == 1 and "NULL pointer gO" in binding.last_error()
+    q = list(p); q[9] = q[0]
+    assert call(q) == 1 and "overlaps input Q" in binding.last_error()
+    q = list(p); q[7] = q[6] + 1024
+    assert call(q) == 1 and "overlap" in binding.last_error()
+    assert call(p, D=80) == 2 and "head_dim" in binding.last_error()
+    three = [(8, 0, 1, 0, 0), (16, 1, 2, 0, 0), (24, 0, 1, 0, 0), (32, 1, 2, 0, 0), (64, 0, 1, 0, 0)]
+    assert call(p, layout=make_layout("ranges", three)) == 2 and "two query ranges" in binding.last_error()
 
 
 @_no_gpu
