@@ -40,7 +40,8 @@ METRIC = "masked attention fwd+JVP TFLOP/s (unmasked pairs) and % bf16 MFMA peak
 # MI355X dense bf16 matrix peak: 256 CUs x 2.4 GHz x 4096 flop/clk/CU
 PEAK_BF16_TFLOPS = 256 * 2.4e9 * 4096 / 1e12
 PEAK_FP32_TFLOPS = 157.3
-KERNEL_SOURCES = ["paper_2606_25473_amd/csrc/attn_mfma.hip", "paper_2606_25473_amd/csrc/schedule.hpp",
+KERNEL_SOURCES = ["paper_2606_25473_amd/csrc/attn_mfma.hip", "paper_2606_25473_amd/csrc/attn_bwd.hip",
+                  "paper_2606_25473_amd/csrc/mfma_common.hpp", "paper_2606_25473_amd/csrc/schedule.hpp",
                   "paper_2606_25473_amd/csrc/kernels.hpp"]
 
 

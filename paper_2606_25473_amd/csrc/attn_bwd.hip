@@ -173,19 +173,20 @@ void attn_bwd_dq_kernel(const BwdArgs a) {
       GP = mfma(*(const bf16x8*)(cV + off), gop[s], GP);
     }
     // P^T = exp(S^T - LSE) on admissible pairs, gS^T = P^T o (gP^T - Delta)
-    float gs[16];
-    const bool full = block_is_full(plan, k0, QBC, L);
+    float p[16], gs[16];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      float p = __builtin_amdgcn_exp2f(fmaf(S[i], c2, -lse2));
-      if (!full) {
+    for (int i = 0; i < 16; ++i) p[i] = __builtin_amdgcn_exp2f(fmaf(S[i], c2, -lse2));
+    if (!block_is_full(plan, k0, QBC, L)) {  // one uniform branch around the whole mask
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
         const int key = k0 + 8 * (i >> 2) + 4 * hh + (i & 3);
         const bool ok = (unsigned)(key - ra0) < (unsigned)(ra1 - ra0) ||
                         (unsigned)(key - rb0) < (unsigned)(rb1 - rb0);
-        p = ok ? p : 0.f;
+        p[i] = ok ? p[i] : 0.f;
       }
-      gs[i] = p * (GP[i] - delta);
     }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) gs[i] = p[i] * (GP[i] - delta);
     // gQ^T += K^T gS^T (K^T from transposed LDS reads, gS^T from this lane's registers)
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -376,34 +377,36 @@ void attn_bwd_dkdv_kernel(const BwdArgs a) {
       S = mfma(*(const bf16x8*)(cs + aoff), *(const bf16x8*)(sK + boff), S);
       GP = mfma(*(const bf16x8*)(cs + G::QTB + aoff), *(const bf16x8*)(sV + boff), GP);
     }
-    // LSE and Delta of the lane's 16 rows (4 runs of 4 consecutive rows)
+    // LSE and Delta of the lane's 16 rows (4 runs of 4 consecutive rows).  A row without
+    // admissible keys has LSE = -inf: exp2 then gives +inf, which the mask (such a row is
+    // never in a full block) replaces by 0.
     const float* sl = (const float*)(cs + 2 * G::QTB);
     const float* sd = sl + QB;
-    float p[16], gs[16];
-    const bool full = block_is_full(plan, q0b, QB, L);
+    float p[16], dl[16];
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const int r = 32 * qh + 8 * c + 4 * hh;
-      const float4 lv = *(const float4*)(sl + r);
-      const float4 dv = *(const float4*)(sd + r);
+      const float4 lv = *(const float4*)(sl + 32 * qh + 8 * c + 4 * hh);
+      const float4 dv = *(const float4*)(sd + 32 * qh + 8 * c + 4 * hh);
       const float lsev[4] = {lv.x, lv.y, lv.z, lv.w};
       const float dlv[4] = {dv.x, dv.y, dv.z, dv.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int i = 4 * c + e;
-        // rows without admissible keys (LSE = -inf) are masked for every key
-        const float l2 = lsev[e] == -INFINITY ? 0.f : lsev[e] * kLog2e;
-        float pv = __builtin_amdgcn_exp2f(fmaf(S[i], c2, -l2));
-        if (!full) {
-          const int q = q0b + r + e;
-          const bool ok = (unsigned)(q - ra0) < (unsigned)(ra1 - ra0) ||
-                          (unsigned)(q - rb0) < (unsigned)(rb1 - rb0);
-          pv = ok ? pv : 0.f;
-        }
-        p[i] = pv;
-        gs[i] = pv * (GP[i] - dlv[e]);
+        p[4 * c + e] = __builtin_amdgcn_exp2f(fmaf(S[4 * c + e], c2, -lsev[e] * kLog2e));
+        dl[4 * c + e] = dlv[e];
       }
     }
+    if (!block_is_full(plan, q0b, QB, L)) {  // one uniform branch around the whole mask
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int q = q0b + 32 * qh + 8 * (i >> 2) + 4 * hh + (i & 3);
+        const bool ok = (unsigned)(q - ra0) < (unsigned)(ra1 - ra0) ||
+                        (unsigned)(q - rb0) < (unsigned)(rb1 - rb0);
+        p[i] = ok ? p[i] : 0.f;
+      }
+    }
+    float gs[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) gs[i] = p[i] * (GP[i] - dl[i]);
     // gV^T += gO^T P and gK^T += Q^T gS (transposed LDS reads of the block's rows)
 #pragma unroll
     for (int t = 0; t < 2; ++t) {

@@ -1,7 +1,7 @@
 """Summarise rocprofv3 CSV output of a bench.py run into a short text report.
 
     python -m paper_2606_25473_amd.profile_summary --trace DIR [--fetch DIR --write DIR]
-        [--copy-mib N] [--workload NAME] [--op jvp|fwd|zc] [--record profiles/hbm_traffic.json]
+        [--copy-mib N] [--workload NAME] [--op jvp|fwd|zc|bwd|bwd_dq] [--record profiles/hbm_traffic.json]
 
 --trace: a ``rocprofv3 --kernel-trace --stats -f csv`` output directory;
 --fetch/--write: ``rocprofv3 --pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE`` output
@@ -19,13 +19,16 @@ import os
 import re
 import statistics
 
-# template mode of attn_mfma_kernel<D, mode> for each op
-OP_MODE = {"fwd": 0, "jvp": 1, "zc": 2}
+# the bf16 kernel whose counters stand for each op: attn_mfma_kernel<D, mode> for the
+# forward, JVP and zero-clean JVP; the key-tile pass (the longer one) for the backward
+OP_KERNEL = {"fwd": r"attn_mfma_kernel<\d+, 0>", "jvp": r"attn_mfma_kernel<\d+, 1>",
+             "zc": r"attn_mfma_kernel<\d+, 2>", "bwd": r"attn_bwd_dkdv_kernel<\d+>",
+             "bwd_dq": r"attn_bwd_dq_kernel<\d+>"}
 
 
 def attn_kernel_of(op):
     """Predicate on rocprofv3 kernel names selecting the bf16 kernel of ``op``."""
-    pat = re.compile(r"attn_mfma_kernel<\d+, %d>" % OP_MODE[op])
+    pat = re.compile(OP_KERNEL[op])
     return lambda name: bool(pat.search(name))
 
 
@@ -68,7 +71,7 @@ def main(argv=None):
     ap.add_argument("--write")
     ap.add_argument("--copy-mib", type=int, default=0)
     ap.add_argument("--workload", default="wan1.3b_chunkwise_tf")
-    ap.add_argument("--op", default="jvp", choices=["jvp", "fwd", "zc"])
+    ap.add_argument("--op", default="jvp", choices=sorted(OP_KERNEL))
     ap.add_argument("--record")
     ap.add_argument("--pmc", nargs="*", default=[], help="counter-collection output dirs to list")
     a = ap.parse_args(argv)
