@@ -48,27 +48,6 @@ struct QGeo {
   static constexpr int IPT = TILEB / 1024;      // 1 KiB direct loads per tile
 };
 
-// Per-lane offsets of the transposed operand reads (ds_read_b64_tr_b16) of a 32-row
-// tile whose rows are listed in the accumulator order of a 32x32 MFMA output:
-// tro[t][p][dt] for k step t (16 rows), row half p (+0 / +8), d tile dt.  In each
-// 16-lane group, lane j receives element j%4 of the 8-byte word addressed by lane
-// 4e + j/4 (e = result element); the addresses below make the row order of the
-// operand equal to that of the B operand taken from the lane's own accumulator.
-template <int D>
-__device__ __forceinline__ void tr_offsets(int lane, int tro[2][2][D / 32]) {
-  const int g16 = lane >> 4, s16 = lane & 15;
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int p = 0; p < 2; ++p)
-#pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt) {
-        const int r = 16 * t + 8 * p + 4 * (g16 >> 1) + (s16 >> 2);
-        const int chunk = 4 * dt + 2 * (g16 & 1) + ((s16 & 3) >> 1);
-        tro[t][p][dt] = lds_off<D>(r, chunk) + 8 * (s16 & 1);
-      }
-}
-
 template <int D>
 __global__ __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_bwd_dq_kernel(const BwdArgs a) {

@@ -19,7 +19,7 @@
 // ds_read_b64_tr_b16, which returns, in each 16-lane group, lane j <- element
 // j%4 of the 8-byte word addressed by lane 4e + j/4 (e = result element).
 //
-// Contractions per wave and 32-key block (D = 128, 32 MFMAs of 32x32x16 = 1 per
+// Contractions per wave and 32-key block (D = 128: 48 MFMAs of 32x32x16, one per
 // 16 keys x 32 d x 32 queries):
 //   S^T  = K Q^T                     8       (2D flop / pair)
 //   dS^T = dK Q^T + K dQ^T          16       (4D)
@@ -34,6 +34,11 @@
 // only when a row's block max exceeds the stored max by more than kLazy (in
 // log2 units), so P~ <= 2^kLazy; the result is the same function, since O, T, l
 // and r always share one reference max.
+//
+// Three kernels come from one body: the forward only (kFwd), the JVP (kJvp) and the
+// JVP with zero tangents on the clean half of a teacher-forcing sequence
+// (kZeroClean); the block loop runs in lockstep (JVP) or ping-pong order (the
+// others), as described at the loop.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -206,7 +211,8 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   };
 
   // per-lane LDS offsets of the transposed V / dV operand reads:
-  // tro[t][p][dt] for k step t (16 keys), key half p (+0 / +8), d tile dt
+  // tro[t][p][dt] for k step t (16 keys), key half p (+0 / +8), d tile dt (computed
+  // in place rather than by tr_offsets(), which the compiler schedules differently here)
   const int g16 = lane >> 4, s16 = lane & 15;
   int tro[2][2][G::DT];
 #pragma unroll
@@ -268,7 +274,6 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   // Output phase of a block: O^T += V^T P~^T ; T^T += dV^T P~^T + V^T H~^T
   auto ophase = [&](auto tk, const char* cV, const char* cdV, const bf16x8* pb, const bf16x8* hb) {
     constexpr bool TK = JVP && decltype(tk)::value;
-    // ---- O^T += V^T P~^T ; T^T += dV^T P~^T + V^T H~^T
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
 #pragma unroll
@@ -284,7 +289,6 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
         }
       }
     }
-
   };
 
   // One key block; TK: the block has tangent keys (dK, dV tiles are present).  Returns
