@@ -333,3 +333,20 @@ def test_python_binding_refuses_cpu_tensors():
     x = torch.zeros(1, 1, 8, 64)
     with pytest.raises(ValueError):
         binding.attn_jvp_fwd(x, x, x, x, x, x, "full")
+
+
+def test_header_compiles_as_c_and_links(lib, tmp_path):
+    """The ABI is usable from plain C: tests/c/abi_check.c compiled with gcc -std=c99
+    against include/attn_jvp.h, linked to the library, run (host-only calls)."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    libdir = os.path.dirname(binding.library_path())
+    exe = str(tmp_path / "abi_check")
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.join(root, "include"),
+                    os.path.join(root, "tests", "c", "abi_check.c"), "-L", libdir, "-lattnjvp",
+                    "-Wl,-rpath," + libdir, "-o", exe], check=True)
+    out = subprocess.run([exe], capture_output=True, text=True)
+    assert out.returncode == 0 and out.stdout.strip() == "OK", out.stdout + out.stderr
