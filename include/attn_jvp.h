@@ -183,8 +183,9 @@ int64_t attn_count_computed_pairs(const attn_chunk_layout* layout, int L, int D)
  * buffer. */
 int attn_query_groups(const attn_chunk_layout* layout, int L, int32_t* out, int max_groups);
 
-/* Host only.  Shape of the work decomposition of the bf16 kernels: query rows
- * per work-group tile and keys per streamed key block. */
+/* Host only.  Shape of the work decomposition of the bf16 JVP kernels: query rows
+ * per work-group tile and keys per streamed key block (the forward-only kernel takes
+ * tiles of half as many rows). */
 void attn_tile_shape(int* rows_per_tile, int* keys_per_block);
 
 /* Host only.  Key-block plan of query tile `qtile` (rows [qtile*R, qtile*R + R)

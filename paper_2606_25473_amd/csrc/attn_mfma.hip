@@ -51,10 +51,7 @@ namespace {
 
 using namespace dev;
 
-constexpr int BR = kMfmaBr;
 constexpr int BC = kMfmaBc;
-constexpr int NW = BR / 32;            // waves per work-group, 32 query rows each
-constexpr int NTHREADS = 64 * NW;
 constexpr float kLazy = 8.0f;
 
 template <int D>
@@ -65,7 +62,6 @@ struct Geo {
   static constexpr int DT = D / 32;               // 32-wide d tiles of O^T / T^T
   static constexpr int KS = D / 16;               // 16-deep k steps of the score contraction
   static constexpr int IPT = TILEB / 1024;        // 1 KiB direct-load instructions per key tile
-  static constexpr int IPQ = BR * ROWB / 1024;    // ... per query tile
 };
 
 // Kernel variants.  kZeroClean is the JVP of a sequence whose rows below t0 carry
@@ -87,9 +83,12 @@ struct Tag {
 
 // One work-group's query tile `qtile` of (batch, head) `bh`.  `stages` and `sdQ`
 // are the work-group's LDS buffers (sized for the JVP bodies).
-template <int D, int MODE>
+template <int D, int MODE, int NW>
 __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const int qtile,
                                           char* const stages, char* const sdQ) {
+  // NW waves per work-group, 32 query rows each
+  constexpr int BR = 32 * NW;
+  constexpr int NTHREADS = 64 * NW;
   constexpr bool JVP = MODE != kFwd;
   constexpr bool ZC = MODE == kZeroClean;
   using G = Geo<D>;
@@ -258,7 +257,7 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   // (k+1) mod 3 (whose block, k-2, was last read in interval k-1) during interval k
   // only.  The score phase runs at raised wave priority, so that its MFMAs go first and
   // its softmax overlaps the other wave's output MFMAs.
-  constexpr bool PP = MODE != kJvp;
+  constexpr bool PP = MODE != kJvp && NW == 8;  // (two waves of a work-group per SIMD)
   constexpr int DIST = PP ? 1 : 2;  // prefetch distance in blocks
   const bool late = PP && wave >= NW / 2;
   // barrier of block k: every own load but those of block k+DIST has landed (lockstep:
@@ -266,8 +265,9 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   // none), every LDS read has returned
   auto end_iteration = [&]() {
     constexpr int N = PP ? 0 : (JVP ? 4 : 2) * ((G::IPT + NW - 1) / NW);
-    static_assert(N == 0 || N == 4, "vmcnt immediate below");
+    static_assert(N == 0 || N == 2 || N == 4, "vmcnt immediate below");
     if constexpr (N == 4) asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    else if constexpr (N == 2) asm volatile("s_waitcnt vmcnt(2) lgkmcnt(0)\n\ts_barrier" ::: "memory");
     else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   };
 
@@ -384,8 +384,9 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   const unsigned st_lds = __builtin_amdgcn_readfirstlane(lds_addr(stages));
   if constexpr (JVP) {
     const unsigned dq_lds = __builtin_amdgcn_readfirstlane(lds_addr(sdQ));
+    constexpr int IPQ = BR * G::ROWB / 1024;  // 1 KiB direct loads of the dQ tile
 #pragma unroll
-    for (int j0 = 0; j0 < G::IPQ; j0 += NW) dma_rows_t(dQg, q0, (j0 + wave) * RPI, dq_lds);
+    for (int j0 = 0; j0 < IPQ; j0 += NW) dma_rows_t(dQg, q0, (j0 + wave) * RPI, dq_lds);
   }
   if (nblk > 0) {
     dma_block(plan_block(plan, 0), st_lds);
@@ -491,8 +492,11 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   }
 }
 
-template <int D, int MODE>
-__global__ __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
+// NW = 8 (JVP and zero-clean: 256-row tiles, one work-group and two waves per SIMD per
+// CU) or 4 (forward only: 128-row tiles and a smaller register footprint, so that three
+// work-groups share a CU, three waves per SIMD, and interleave without any schedule).
+template <int D, int MODE, int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW == 8 ? 2 : 3, NW == 8 ? 2 : 3)))
 void attn_mfma_kernel(const AttnArgs a) {
   constexpr bool JVP = MODE != kFwd;
   using G = Geo<D>;
@@ -501,35 +505,36 @@ void attn_mfma_kernel(const AttnArgs a) {
   // two waves per SIMD).  D = 128 JVP: 3 x 32 KiB + 64 KiB = 160 KiB.
   constexpr int SB = JVP ? 4 * G::TILEB : 2 * G::TILEB + 32;
   __shared__ __attribute__((aligned(1024))) char stages[3 * SB];
-  __shared__ __attribute__((aligned(1024))) char sdQ[JVP ? BR * G::ROWB : 16];
+  __shared__ __attribute__((aligned(1024))) char sdQ[JVP ? 32 * NW * G::ROWB : 16];
 
   const int nqt = a.order.nt;
   const int bh = blockIdx.x / nqt;
   const int qtile = tile_of(a.order, blockIdx.x - bh * nqt);
   if constexpr (MODE == kZeroClean) {
-    if ((qtile + 1) * BR <= a.t0) {  // no tangent row in the tile: the primal only
-      tile_body<D, kFwd>(a, bh, qtile, stages, sdQ);
+    if ((qtile + 1) * 32 * NW <= a.t0) {  // no tangent row in the tile: the primal only
+      tile_body<D, kFwd, NW>(a, bh, qtile, stages, sdQ);
       return;
     }
   }
-  tile_body<D, MODE>(a, bh, qtile, stages, sdQ);
+  tile_body<D, MODE, NW>(a, bh, qtile, stages, sdQ);
 }
 
 }  // namespace
 
 hipError_t launch_mfma_bf16(const AttnArgs& a, int D, Pass pass, hipStream_t stream) {
   const dim3 grid((unsigned)(a.order.nt * a.B * a.H));
-  const dim3 block(NTHREADS);
+  constexpr int NJ = kMfmaBr / 32, NF = kMfmaBrFwd / 32;
+  const dim3 block(64 * (pass == Pass::kFwd ? NF : NJ));
   if (D == 128) {
-    if (pass == Pass::kJvp) hipLaunchKernelGGL((attn_mfma_kernel<128, kJvp>), grid, block, 0, stream, a);
+    if (pass == Pass::kJvp) hipLaunchKernelGGL((attn_mfma_kernel<128, kJvp, NJ>), grid, block, 0, stream, a);
     else if (pass == Pass::kJvpZeroClean)
-      hipLaunchKernelGGL((attn_mfma_kernel<128, kZeroClean>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((attn_mfma_kernel<128, kFwd>), grid, block, 0, stream, a);
+      hipLaunchKernelGGL((attn_mfma_kernel<128, kZeroClean, NJ>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((attn_mfma_kernel<128, kFwd, NF>), grid, block, 0, stream, a);
   } else {
-    if (pass == Pass::kJvp) hipLaunchKernelGGL((attn_mfma_kernel<64, kJvp>), grid, block, 0, stream, a);
+    if (pass == Pass::kJvp) hipLaunchKernelGGL((attn_mfma_kernel<64, kJvp, NJ>), grid, block, 0, stream, a);
     else if (pass == Pass::kJvpZeroClean)
-      hipLaunchKernelGGL((attn_mfma_kernel<64, kZeroClean>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((attn_mfma_kernel<64, kFwd>), grid, block, 0, stream, a);
+      hipLaunchKernelGGL((attn_mfma_kernel<64, kZeroClean, NJ>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((attn_mfma_kernel<64, kFwd, NF>), grid, block, 0, stream, a);
   }
   return hipGetLastError();
 }

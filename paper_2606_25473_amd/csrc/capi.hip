@@ -89,8 +89,10 @@ int prepare(attn::Pass pass, int dtype, int B, int H, int L, int D, const void* 
   args->B = B; args->H = H; args->L = L;
   args->t0 = t0;
   args->scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)D);
+  // the forward-only bf16 kernel takes 128-row tiles, the JVP kernels 256-row tiles
+  const int br = (pass == attn::Pass::kFwd && dtype == ATTN_DTYPE_BF16) ? attn::kMfmaBrFwd : attn::kMfmaBr;
   args->order = zc ? attn::make_tile_order_zero_clean(args->gt, L, attn::kMfmaBr, attn::kMfmaBc, t0)
-                   : attn::make_tile_order(layout, L, attn::kMfmaBr);
+                   : attn::make_tile_order(layout, L, br);
   return ATTN_OK;
 }
 

@@ -46,8 +46,10 @@ struct BwdArgs {
   TileOrder order;
 };
 
-// bf16 MFMA kernels: query tiles of kMfmaBr rows (8 waves x 32 rows), key blocks of kMfmaBc keys.
+// bf16 MFMA kernels: query tiles of kMfmaBr rows (8 waves x 32 rows) for the JVP kernels,
+// kMfmaBrFwd rows (4 waves) for the forward-only kernel; key blocks of kMfmaBc keys.
 constexpr int kMfmaBr = 256;
+constexpr int kMfmaBrFwd = 128;
 constexpr int kMfmaBc = 32;
 
 // fp32 exact-path kernels: one wave per query row.
