@@ -19,10 +19,10 @@ import os
 import re
 import statistics
 
-# the bf16 kernel whose counters stand for each op: attn_mfma_kernel<D, mode> for the
+# the bf16 kernel whose counters stand for each op: attn_mfma_kernel<D, mode, waves> for the
 # forward, JVP and zero-clean JVP; the key-tile pass (the longer one) for the backward
-OP_KERNEL = {"fwd": r"attn_mfma_kernel<\d+, 0>", "jvp": r"attn_mfma_kernel<\d+, 1>",
-             "zc": r"attn_mfma_kernel<\d+, 2>", "bwd": r"attn_bwd_dkdv_kernel<\d+>",
+OP_KERNEL = {"fwd": r"attn_mfma_kernel<\d+, 0, \d+>", "jvp": r"attn_mfma_kernel<\d+, 1, \d+>",
+             "zc": r"attn_mfma_kernel<\d+, 2, \d+>", "bwd": r"attn_bwd_dkdv_kernel<\d+>",
              "bwd_dq": r"attn_bwd_dq_kernel<\d+>"}
 
 
