@@ -62,9 +62,9 @@ void attn_bwd_dq_kernel(const BwdArgs a) {
   const int hh = lane >> 5;
   const int L = a.L;
 
-  const int nqt = a.order.nt;
-  const int bh = blockIdx.x / nqt;
-  const int qtile = tile_of(a.order, blockIdx.x - bh * nqt);
+  const TileSlot sl = slot_of(blockIdx.x, a.B * a.H, a.order.nt);
+  const int bh = sl.bh;
+  const int qtile = tile_of(a.order, sl.pos);
   const size_t head = (size_t)bh * L * D;
   const bf16_t* __restrict__ Qg = (const bf16_t*)a.Q + head;
   const bf16_t* __restrict__ Kg = (const bf16_t*)a.K + head;
@@ -268,9 +268,9 @@ void attn_bwd_dkdv_kernel(const BwdArgs a) {
   const int qh = wave >> 2;  // which 32 rows of each query block
   const int L = a.L;
 
-  const int nkt = a.order.nt;
-  const int bh = blockIdx.x / nkt;
-  const int ktile = tile_of(a.order, blockIdx.x - bh * nkt);
+  const TileSlot sl = slot_of(blockIdx.x, a.B * a.H, a.order.nt);
+  const int bh = sl.bh;
+  const int ktile = tile_of(a.order, sl.pos);
   const size_t head = (size_t)bh * L * D;
   const bf16_t* __restrict__ Qg = (const bf16_t*)a.Q + head;
   const bf16_t* __restrict__ Kg = (const bf16_t*)a.K + head;

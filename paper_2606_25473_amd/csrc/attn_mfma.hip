@@ -507,9 +507,9 @@ void attn_mfma_kernel(const AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) char stages[3 * SB];
   __shared__ __attribute__((aligned(1024))) char sdQ[JVP ? 32 * NW * G::ROWB : 16];
 
-  const int nqt = a.order.nt;
-  const int bh = blockIdx.x / nqt;
-  const int qtile = tile_of(a.order, blockIdx.x - bh * nqt);
+  const TileSlot sl = slot_of(blockIdx.x, a.B * a.H, a.order.nt);
+  const int bh = sl.bh;
+  const int qtile = tile_of(a.order, sl.pos);
   if constexpr (MODE == kZeroClean) {
     if ((qtile + 1) * 32 * NW <= a.t0) {  // no tangent row in the tile: the primal only
       tile_body<D, kFwd, NW>(a, bh, qtile, stages, sdQ);

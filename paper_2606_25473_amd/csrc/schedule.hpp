@@ -166,4 +166,27 @@ ATTN_HD int tile_of(const TileOrder& o, int t) {
   return t;
 }
 
+// Work-group b of a launch over nbh (batch, head) pairs and nt tiles per pair: the pairs
+// form groups of kHeadGroup, taken one group after another; inside a group, work-groups
+// go position-major (every pair's first tile of the order, then every pair's second, ...).
+// So the heaviest tiles of a group's heads are dispatched first, before any light one,
+// and a run never ends on a few long tiles of the last head (heads one after another
+// leave such a tail); and no more than about kHeadGroup heads' keys and values are in
+// flight at once, which keeps the caches useful for launches over many heads.
+constexpr int kHeadGroup = 12;
+
+struct TileSlot {
+  int bh, pos;
+};
+
+ATTN_HD TileSlot slot_of(int b, int nbh, int nt) {
+  const int grp = b / (kHeadGroup * nt);
+  const int gsz = imin(kHeadGroup, nbh - grp * kHeadGroup);
+  const int r = b - grp * kHeadGroup * nt;
+  TileSlot s;
+  s.pos = r / gsz;
+  s.bh = grp * kHeadGroup + (r - s.pos * gsz);
+  return s;
+}
+
 }  // namespace attn

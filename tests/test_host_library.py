@@ -350,3 +350,19 @@ def test_header_compiles_as_c_and_links(lib, tmp_path):
                     "-Wl,-rpath," + libdir, "-o", exe], check=True)
     out = subprocess.run([exe], capture_output=True, text=True)
     assert out.returncode == 0 and out.stdout.strip() == "OK", out.stdout + out.stderr
+
+
+def test_schedule_helpers_on_the_host(tmp_path):
+    """The work-group -> (batch-head, tile) slots and the tile orders that the kernels
+    evaluate (schedule.hpp, compiled here with g++) are permutations."""
+    import shutil
+    import subprocess
+    if shutil.which("g++") is None:
+        pytest.skip("g++ not available")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    exe = str(tmp_path / "schedule_check")
+    subprocess.run(["g++", "-std=c++17", "-O1", "-Wall", "-Werror",
+                    "-I", os.path.join(root, "paper_2606_25473_amd", "csrc"),
+                    os.path.join(root, "tests", "c", "schedule_check.cpp"), "-o", exe], check=True)
+    out = subprocess.run([exe], capture_output=True, text=True)
+    assert out.returncode == 0 and out.stdout.strip() == "OK", out.stdout + out.stderr
