@@ -289,6 +289,9 @@ def main():
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_TFLOPS
     prof = profile_record(w.name, mode)
     traffic = prof.get("hbm_bytes_per_launch")
+    if mode == "bwd" and traffic is not None:
+        # a backward call is two launches; the record of the first (query-tile) pass is separate
+        traffic = traffic + profile_record(w.name, "bwd_dq").get("hbm_bytes_per_launch", float("nan"))
     res = {
         "metric": MODE_METRIC[mode],
         "value": round(value, 3),
