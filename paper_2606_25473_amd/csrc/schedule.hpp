@@ -171,9 +171,9 @@ ATTN_HD int tile_of(const TileOrder& o, int t) {
 // go position-major (every pair's first tile of the order, then every pair's second, ...).
 // So the heaviest tiles of a group's heads are dispatched first, before any light one,
 // and a run never ends on a few long tiles of the last head (heads one after another
-// leave such a tail); and no more than about kHeadGroup heads' keys and values are in
-// flight at once, which keeps the caches useful for launches over many heads.
-constexpr int kHeadGroup = 12;
+// leave such a tail); and only about kHeadGroup heads' keys and values are in flight at
+// once, which keeps the caches useful (all heads at once slowed launches over many heads).
+constexpr int kHeadGroup = 4;
 
 struct TileSlot {
   int bh, pos;
