@@ -93,10 +93,13 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   constexpr bool ZC = MODE == kZeroClean;
   using G = Geo<D>;
   constexpr int TB = G::TILEB;
-  constexpr int TBJ = JVP ? G::TILEB : 16;      // tangent tiles exist only in the JVP bodies
+  constexpr int TBJ = JVP ? G::TILEB : 0;       // tangent tiles exist only in the JVP bodies
   // Three pipeline stages (block k is read from stage k mod 3 while block k+2 streams
   // into stage (k+2) mod 3), each holding the K, V, dK, dV tiles of one key block.
   constexpr int SB = 2 * TB + 2 * TBJ;
+  // (operand addresses below are formed by XOR of the in-tile offsets, which needs
+  // tile bases aligned beyond the tile-row size)
+  static_assert(SB % 1024 == 0 && TB % 1024 == 0, "LDS tiles must be 1 KiB aligned");
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
@@ -209,21 +212,16 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
     for (int c = tid; c < n; c += NTHREADS) *(u32x4*)(base + 16 * c) = u32x4{0u, 0u, 0u, 0u};
   };
 
-  // per-lane LDS offsets of the transposed V / dV operand reads:
-  // tro[t][p][dt] for k step t (16 keys), key half p (+0 / +8), d tile dt (computed
-  // in place rather than by tr_offsets(), which the compiler schedules differently here)
+  // Per-lane LDS offsets of the MFMA operand reads.  With the row swizzle, the offset of
+  // chunk 2s + hh of a row is lds_off(row, hh) ^ (32 s), and the transposed V / dV read
+  // for k step t (16 keys), key half p (+0 / +8) and d tile dt is at
+  // 16 t ROWB + (trx[p] ^ (64 dt)) (lane l of a 16-lane group reads 8 bytes addressed for
+  // lane 4e + l/4, e = result element).  Only these bases stay in registers; the per-step
+  // offsets cost one XOR each.
   const int g16 = lane >> 4, s16 = lane & 15;
-  int tro[2][2][G::DT];
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int p = 0; p < 2; ++p)
-#pragma unroll
-      for (int dt = 0; dt < G::DT; ++dt) {
-        const int r = 16 * t + 8 * p + 4 * (g16 >> 1) + (s16 >> 2);
-        const int chunk = 4 * dt + 2 * (g16 & 1) + ((s16 & 3) >> 1);
-        tro[t][p][dt] = lds_off<D>(r, chunk) + 8 * (s16 & 1);
-      }
+  const int tr_r = 4 * (g16 >> 1) + (s16 >> 2), tr_c = 2 * (g16 & 1) + ((s16 & 3) >> 1);
+  const unsigned trx0 = lds_off<D>(tr_r, tr_c) + 8 * (s16 & 1);
+  const unsigned trx1 = lds_off<D>(8 + tr_r, tr_c) + 8 * (s16 & 1);
 
   // ---- accumulators (O^T, T^T: lane holds query l%32, d = 32 dt + 8 (i/4) + 4 (l/32) + i%4)
   f32x16 oacc[G::DT], tacc[JVP ? G::DT : 1];
@@ -239,6 +237,7 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   const float c2 = a.scale * kLog2e;
   const float sc = a.scale;
   const int krow = lane & 31;
+  const unsigned koff = lds_off<D>(krow, hh), dqoff = lds_off<D>(qrow, hh);
 
   // Two schedules of the key-block loop, both with three LDS stages.
   //
@@ -271,23 +270,35 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
     else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   };
 
-  // Output phase of a block: O^T += V^T P~^T ; T^T += dV^T P~^T + V^T H~^T
+  // Output phase of a block: O^T += V^T P~^T ; T^T += dV^T P~^T + V^T H~^T, one (t, dt)
+  // group of MFMAs at a time, its operands read OPF groups ahead (the order is pinned with
+  // scheduling fences: left to itself the compiler waits on each read right before its
+  // MFMA)
   auto ophase = [&](auto tk, const char* cV, const char* cdV, const bf16x8* pb, const bf16x8* hb) {
     constexpr bool TK = JVP && decltype(tk)::value;
+    constexpr int OPF = JVP ? 1 : 2;
+    constexpr int NG = 2 * G::DT;
+    const unsigned vb0 = vreg_add(lds_addr(cV), trx0), vb1 = vreg_add(lds_addr(cV), trx1);
+    const unsigned dvo = (unsigned)(cdV - cV);
+    bf16x8 vop[OPF + 1], dvop[OPF + 1];
+    auto read = [&](int g) {
+      const int t = g / G::DT, dt = g % G::DT, b = g % (OPF + 1);
+      const unsigned o = 16u * t * G::ROWB;
+      const unsigned a0 = vb0 ^ (64u * dt), a1 = vb1 ^ (64u * dt);
+      vop[b] = cat(ld_tr_at(a0 + o), ld_tr_at(a1 + o));
+      if constexpr (TK) dvop[b] = cat(ld_tr_at(a0 + o + dvo), ld_tr_at(a1 + o + dvo));
+    };
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
+    for (int g = 0; g < OPF; ++g) read(g);
 #pragma unroll
-      for (int dt = 0; dt < G::DT; ++dt) {
-        const bf16x8 vop = cat(ld_tr(cV + tro[t][0][dt]), ld_tr(cV + tro[t][1][dt]));
-        oacc[dt] = mfma(vop, pb[t], oacc[dt]);
-        if constexpr (JVP) {
-          if constexpr (TK) {
-            const bf16x8 dvop = cat(ld_tr(cdV + tro[t][0][dt]), ld_tr(cdV + tro[t][1][dt]));
-            tacc[dt] = mfma(dvop, pb[t], tacc[dt]);
-          }
-          tacc[dt] = mfma(vop, hb[t], tacc[dt]);
-        }
-      }
+    for (int g = 0; g < NG; ++g) {
+      if (g + OPF < NG) read(g + OPF);
+      __builtin_amdgcn_sched_barrier(0);
+      const int t = g / G::DT, dt = g % G::DT, b = g % (OPF + 1);
+      oacc[dt] = mfma(vop[b], pb[t], oacc[dt]);
+      if constexpr (TK) tacc[dt] = mfma(dvop[b], pb[t], tacc[dt]);
+      if constexpr (JVP) tacc[dt] = mfma(vop[b], hb[t], tacc[dt]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
@@ -310,19 +321,31 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
     // ---- scores and score tangents (transposed): S^T = K Q^T, dS^T = dK Q^T + K dQ^T
     if constexpr (PP) __builtin_amdgcn_s_setprio(1);
     f32x16 S = f32x16{}, dS = f32x16{};
+    // operand reads run SPF k steps ahead of the MFMAs that consume them (order pinned
+    // with scheduling fences, as in the output phase); the dQ base is recomputed per
+    // iteration (vreg_add with the iteration as a dependency) like the stage-relative ones
+    constexpr int SPF = JVP ? 1 : 2;
+    const unsigned kb = vreg_add(lds_addr(cK), koff);
+    const unsigned dqb = vreg_add(lds_addr(sdQ), dqoff, it);
+    const unsigned dko = (unsigned)(cdK - cK);
+    bf16x8 kop[SPF + 1], dkop[SPF + 1], dqop[SPF + 1];
+    auto read = [&](int s) {
+      const int b = s % (SPF + 1);
+      kop[b] = ld128_at(kb ^ (32u * s));
+      if constexpr (TK) dkop[b] = ld128_at((kb ^ (32u * s)) + dko);
+      if constexpr (JVP) dqop[b] = ld128_at(dqb ^ (32u * s));
+    };
+#pragma unroll
+    for (int s = 0; s < SPF; ++s) read(s);
 #pragma unroll
     for (int s = 0; s < G::KS; ++s) {
-      const int off = lds_off<D>(krow, 2 * s + hh);
-      const bf16x8 kop = *(const bf16x8*)(cK + off);
-      S = mfma(kop, qop[s], S);
-      if constexpr (JVP) {
-        const bf16x8 dqop = *(const bf16x8*)(sdQ + lds_off<D>(qrow, 2 * s + hh));
-        if constexpr (TK) {
-          const bf16x8 dkop = *(const bf16x8*)(cdK + off);
-          dS = mfma(dkop, qop[s], dS);
-        }
-        dS = mfma(kop, dqop, dS);
-      }
+      if (s + SPF < G::KS) read(s + SPF);
+      __builtin_amdgcn_sched_barrier(0);
+      const int b = s % (SPF + 1);
+      S = mfma(kop[b], qop[s], S);
+      if constexpr (TK) dS = mfma(dkop[b], qop[s], dS);
+      if constexpr (JVP) dS = mfma(kop[b], dqop[b], dS);
+      __builtin_amdgcn_sched_barrier(0);
     }
 
     // ---- mask (only on blocks not admissible for every row of the tile): S = -inf, dS = 0

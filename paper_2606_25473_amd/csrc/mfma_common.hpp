@@ -43,6 +43,30 @@ __device__ __forceinline__ bf16x4 ld_tr(const char* p) {
   return __builtin_bit_cast(bf16x4, v);
 }
 
+// The same reads from a 32-bit LDS byte address (ds_read_b64_tr_b16 / ds_read_b128).
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+__device__ __forceinline__ bf16x4 ld_tr_at(unsigned addr) {
+  return __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(uintptr_t)addr));
+}
+__device__ __forceinline__ bf16x8 ld128_at(unsigned addr) { return *(lds_bf16x8*)(uintptr_t)addr; }
+
+// u + v in a vector register, opaque to the compiler.  Offsets derived from the result
+// (one XOR per operand read) are then formed where they are used instead of being
+// hoisted out of the key-block loop, where each would hold a register for the whole
+// loop.  The optional `dep` (unused by the instruction) ties the result to a loop-variant
+// value when u and v are loop-invariant.
+__device__ __forceinline__ unsigned vreg_add(unsigned u, unsigned v) {
+  unsigned r;
+  asm("v_add_u32 %0, %1, %2" : "=v"(r) : "s"(u), "v"(v));
+  return r;
+}
+__device__ __forceinline__ unsigned vreg_add(unsigned u, unsigned v, int dep) {
+  unsigned r;
+  asm("v_add_u32 %0, %1, %2 ; %3" : "=v"(r) : "s"(u), "v"(v), "s"(dep));
+  return r;
+}
+
 __device__ __forceinline__ bf16x8 cat(bf16x4 a, bf16x4 b) {
   return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
 }
