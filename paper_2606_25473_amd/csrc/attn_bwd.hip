@@ -126,14 +126,16 @@ void attn_bwd_dq_kernel(const BwdArgs a) {
     dma_tile(Vg, kb * QBC, st + TB);
   };
 
-  int tro[2][2][G::DT];
-  tr_offsets<D>(lane, tro);
+  static_assert(SB % 1024 == 0 && TB % 1024 == 0, "LDS tiles must be 1 KiB aligned");
+  unsigned trx[2];
+  tr_bases<D>(lane, trx);
 
   f32x16 gacc[G::DT];
 #pragma unroll
   for (int dt = 0; dt < G::DT; ++dt) gacc[dt] = f32x16{};
   const float c2 = a.scale * kLog2e;
   const int krow = lane & 31;
+  const unsigned koff = lds_off<D>(krow, hh);  // chunk 2s + hh of the row: koff ^ (32 s)
 
   // wait for every load but this iteration's prefetch (2 per wave at D = 128; at D = 64
   // waves 0..3 issue one per tile and the others none), then synchronise
@@ -143,13 +145,29 @@ void attn_bwd_dq_kernel(const BwdArgs a) {
   auto step = [&](int it, const char* cK, const char* cV, unsigned next_stage) {
     dma_block(plan_block(plan, min(it + 2, nblk - 1)), next_stage);
     const int k0 = plan_block(plan, it) * QBC;
-    // S^T = K Q^T and gP^T = V gO^T (lane: query l%32, keys 8 (i/4) + 4 (l/32) + i%4)
+    // S^T = K Q^T and gP^T = V gO^T (lane: query l%32, keys 8 (i/4) + 4 (l/32) + i%4);
+    // operand reads run SPF k steps ahead of their MFMAs (order pinned with scheduling
+    // fences)
     f32x16 S = f32x16{}, GP = f32x16{};
+    constexpr int SPF = 2;
+    const unsigned kb = vreg_add(lds_addr(cK), koff);
+    const unsigned vo = (unsigned)(cV - cK);
+    bf16x8 kop[SPF + 1], vop[SPF + 1];
+    auto read = [&](int s) {
+      const int b = s % (SPF + 1);
+      kop[b] = ld128_at(kb ^ (32u * s));
+      vop[b] = ld128_at((kb ^ (32u * s)) + vo);
+    };
+#pragma unroll
+    for (int s = 0; s < SPF; ++s) read(s);
 #pragma unroll
     for (int s = 0; s < G::KS; ++s) {
-      const int off = lds_off<D>(krow, 2 * s + hh);
-      S = mfma(*(const bf16x8*)(cK + off), qop[s], S);
-      GP = mfma(*(const bf16x8*)(cV + off), gop[s], GP);
+      if (s + SPF < G::KS) read(s + SPF);
+      __builtin_amdgcn_sched_barrier(0);
+      const int b = s % (SPF + 1);
+      S = mfma(kop[b], qop[s], S);
+      GP = mfma(vop[b], gop[s], GP);
+      __builtin_amdgcn_sched_barrier(0);
     }
     // P^T = exp(S^T - LSE) on admissible pairs, gS^T = P^T o (gP^T - Delta)
     float p[16], gs[16];
@@ -166,17 +184,29 @@ void attn_bwd_dq_kernel(const BwdArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < 16; ++i) gs[i] = p[i] * (GP[i] - delta);
-    // gQ^T += K^T gS^T (K^T from transposed LDS reads, gS^T from this lane's registers)
+    // gQ^T += K^T gS^T (K^T from transposed LDS reads, gS^T from this lane's registers),
+    // one (t, dt) MFMA at a time with its operand read OPF groups ahead
+    bf16x8 gsb[2];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      bf16x8 gsb;
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) gsb[j] = (bf16_t)gs[8 * t + j];
+      for (int j = 0; j < 8; ++j) gsb[t][j] = (bf16_t)gs[8 * t + j];
+    constexpr int OPF = 2, NG = 2 * G::DT;
+    const unsigned tb0 = vreg_add(lds_addr(cK), trx[0]), tb1 = vreg_add(lds_addr(cK), trx[1]);
+    bf16x8 kt[OPF + 1];
+    auto read_t = [&](int g) {
+      const int t = g / G::DT, dt = g % G::DT;
+      const unsigned o = 16u * t * G::ROWB;
+      kt[g % (OPF + 1)] = cat(ld_tr_at((tb0 ^ (64u * dt)) + o), ld_tr_at((tb1 ^ (64u * dt)) + o));
+    };
 #pragma unroll
-      for (int dt = 0; dt < G::DT; ++dt) {
-        const bf16x8 kt = cat(ld_tr(cK + tro[t][0][dt]), ld_tr(cK + tro[t][1][dt]));
-        gacc[dt] = mfma(kt, gsb, gacc[dt]);
-      }
+    for (int g = 0; g < OPF; ++g) read_t(g);
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      if (g + OPF < NG) read_t(g + OPF);
+      __builtin_amdgcn_sched_barrier(0);
+      gacc[g % G::DT] = mfma(kt[g % (OPF + 1)], gsb[g / G::DT], gacc[g % G::DT]);
+      __builtin_amdgcn_sched_barrier(0);
     }
     end_iteration();
   };
@@ -257,7 +287,6 @@ void attn_bwd_dkdv_kernel(const BwdArgs a) {
   using G = KGeo<D>;
   __shared__ __attribute__((aligned(1024))) char lds[G::BYTES];
   char* const sK = lds;
-  char* const sV = lds + G::KTB;
   char* const stages = lds + 2 * G::KTB;
 
   const int tid = threadIdx.x;
@@ -321,9 +350,13 @@ void attn_bwd_dkdv_kernel(const BwdArgs a) {
     if (wave == NW - 1) lds_load4(Dg, roff, st + 2 * G::QTB + 4 * QB);
   };
 
-  int tro[2][2][G::DT];
-  tr_offsets<D>(lane, tro);
+  static_assert(G::SB % 256 == 0 && G::KTB % 1024 == 0, "XOR-formed offsets need row-aligned tiles");
+  unsigned trx[2];
+  tr_bases<D>(lane, trx);
   const int qoff = qh * 32 * G::ROWB;  // this wave's 32 rows within a query block tile
+  // chunk 2s + hh of a row sits at the row's chunk-hh offset ^ (32 s)
+  const unsigned qaoff = qoff + lds_off<D>(lane & 31, hh);
+  const unsigned kboff = lds_addr(sK) + lds_off<D>(krow, hh);
 
   f32x16 gk[G::DT], gv[G::DT];
 #pragma unroll
@@ -347,14 +380,27 @@ void attn_bwd_dkdv_kernel(const BwdArgs a) {
     if (it + 1 < nblk) dma_qblock(plan_block(plan, it + 1), st_lds + (unsigned)(((it + 1) & 1) * G::SB));
     const int q0b = plan_block(plan, it) * QB;
 
-    // S = Q K^T and gP = gO V^T (lane: key l%32, rows 8 (i/4) + 4 (l/32) + i%4 of the half)
+    // S = Q K^T and gP = gO V^T (lane: key l%32, rows 8 (i/4) + 4 (l/32) + i%4 of the
+    // half); operand reads one k step ahead of their MFMAs (order pinned with fences)
     f32x16 S = f32x16{}, GP = f32x16{};
+    const unsigned qa = vreg_add(lds_addr(cs), qaoff);
+    const unsigned kb = vreg_add(0u, kboff, it);
+    bf16x8 aq[2], ag[2], bk[2], bv[2];
+    auto read = [&](int s) {
+      const unsigned x = 32u * s;
+      aq[s & 1] = ld128_at(qa ^ x);
+      ag[s & 1] = ld128_at((qa ^ x) + G::QTB);
+      bk[s & 1] = ld128_at(kb ^ x);
+      bv[s & 1] = ld128_at((kb ^ x) + G::KTB);
+    };
+    read(0);
 #pragma unroll
     for (int s = 0; s < G::KS; ++s) {
-      const int aoff = qoff + lds_off<D>(lane & 31, 2 * s + hh);
-      const int boff = lds_off<D>(krow, 2 * s + hh);
-      S = mfma(*(const bf16x8*)(cs + aoff), *(const bf16x8*)(sK + boff), S);
-      GP = mfma(*(const bf16x8*)(cs + G::QTB + aoff), *(const bf16x8*)(sV + boff), GP);
+      if (s + 1 < G::KS) read(s + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      S = mfma(aq[s & 1], bk[s & 1], S);
+      GP = mfma(ag[s & 1], bv[s & 1], GP);
+      __builtin_amdgcn_sched_barrier(0);
     }
     // LSE and Delta of the lane's 16 rows (4 runs of 4 consecutive rows).  A row without
     // admissible keys has LSE = -inf: exp2 then gives +inf, which the mask (such a row is
@@ -386,23 +432,35 @@ void attn_bwd_dkdv_kernel(const BwdArgs a) {
     float gs[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) gs[i] = p[i] * (GP[i] - dl[i]);
-    // gV^T += gO^T P and gK^T += Q^T gS (transposed LDS reads of the block's rows)
+    // gV^T += gO^T P and gK^T += Q^T gS (transposed LDS reads of the block's rows), one
+    // (t, dt) group at a time with its operands read one group ahead
+    bf16x8 pb[2], gsb[2];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      bf16x8 pb, gsb;
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        pb[j] = (bf16_t)p[8 * t + j];
-        gsb[j] = (bf16_t)gs[8 * t + j];
+        pb[t][j] = (bf16_t)p[8 * t + j];
+        gsb[t][j] = (bf16_t)gs[8 * t + j];
       }
+    constexpr int NG = 2 * G::DT;
+    const unsigned tb0 = vreg_add(lds_addr(cs + qoff), trx[0]), tb1 = vreg_add(lds_addr(cs + qoff), trx[1]);
+    bf16x8 got[2], qt[2];
+    auto read_t = [&](int g) {
+      const int t = g / G::DT, dt = g % G::DT;
+      const unsigned o = 16u * t * G::ROWB;
+      const unsigned a0 = (tb0 ^ (64u * dt)) + o, a1 = (tb1 ^ (64u * dt)) + o;
+      got[g & 1] = cat(ld_tr_at(a0 + G::QTB), ld_tr_at(a1 + G::QTB));
+      qt[g & 1] = cat(ld_tr_at(a0), ld_tr_at(a1));
+    };
+    read_t(0);
 #pragma unroll
-      for (int dt = 0; dt < G::DT; ++dt) {
-        const char* qs = cs + qoff;
-        const bf16x8 got = cat(ld_tr(qs + G::QTB + tro[t][0][dt]), ld_tr(qs + G::QTB + tro[t][1][dt]));
-        gv[dt] = mfma(got, pb, gv[dt]);
-        const bf16x8 qt = cat(ld_tr(qs + tro[t][0][dt]), ld_tr(qs + tro[t][1][dt]));
-        gk[dt] = mfma(qt, gsb, gk[dt]);
-      }
+    for (int g = 0; g < NG; ++g) {
+      if (g + 1 < NG) read_t(g + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      const int t = g / G::DT, dt = g % G::DT;
+      gv[dt] = mfma(got[g & 1], pb[t], gv[dt]);
+      gk[dt] = mfma(qt[g & 1], gsb[t], gk[dt]);
+      __builtin_amdgcn_sched_barrier(0);
     }
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   }

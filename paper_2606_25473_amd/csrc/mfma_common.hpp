@@ -118,5 +118,16 @@ __device__ __forceinline__ void tr_offsets(int lane, int tro[2][2][D / 32]) {
       }
 }
 
+// The same offsets as two bases: with the row swizzle, tro[t][p][dt] equals
+// 16 t ROWB + (trx[p] ^ (64 dt)), so a kernel keeps trx[0..1] in registers and forms
+// each read's offset with one XOR.
+template <int D>
+__device__ __forceinline__ void tr_bases(int lane, unsigned trx[2]) {
+  const int g16 = lane >> 4, s16 = lane & 15;
+  const int r = 4 * (g16 >> 1) + (s16 >> 2), chunk = 2 * (g16 & 1) + ((s16 & 3) >> 1);
+  trx[0] = lds_off<D>(r, chunk) + 8 * (s16 & 1);
+  trx[1] = lds_off<D>(8 + r, chunk) + 8 * (s16 & 1);
+}
+
 }  // namespace dev
 }  // namespace attn
