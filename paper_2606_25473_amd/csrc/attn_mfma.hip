@@ -37,8 +37,8 @@
 //
 // Three kernels come from one body: the forward only (kFwd), the JVP (kJvp) and the
 // JVP with zero tangents on the clean half of a teacher-forcing sequence
-// (kZeroClean); the block loop runs in lockstep (JVP) or ping-pong order (the
-// others), as described at the loop.
+// (kZeroClean); the block loop runs in lockstep (4-wave forward) or ping-pong order
+// (8-wave JVP kernels), as described at the loop.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -241,12 +241,13 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
 
   // Two schedules of the key-block loop, both with three LDS stages.
   //
-  // Lockstep (the dense JVP): every wave passes the barrier of block k after both
-  // phases of block k.  Block k+2 streams into stage (k+2) mod 3 during iterations k
-  // and k+1 (two iterations of latency hidden).
+  // Lockstep (the 4-wave forward kernel, whose three work-groups per CU interleave by
+  // themselves): every wave passes the barrier of block k after both phases of block k.
+  // Block k+2 streams into stage (k+2) mod 3 during iterations k and k+1 (two
+  // iterations of latency hidden).
   //
-  // Ping-pong (forward-only and zero-clean kernels, whose share of softmax work is
-  // larger): the waves of the first half of the work-group (one per SIMD) pass the
+  // Ping-pong (the 8-wave kernels: JVP, zero-clean JVP): the waves of the first half of
+  // the work-group (one per SIMD) pass the
   // barrier of block k after its output phase, those of the second half after its
   // score phase, so that each SIMD runs one wave's score phase (MFMA, then the softmax
   // on the vector ALU) beside the other wave's output phase:
@@ -256,7 +257,7 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   // (k+1) mod 3 (whose block, k-2, was last read in interval k-1) during interval k
   // only.  The score phase runs at raised wave priority, so that its MFMAs go first and
   // its softmax overlaps the other wave's output MFMAs.
-  constexpr bool PP = MODE != kJvp && NW == 8;  // (two waves of a work-group per SIMD)
+  constexpr bool PP = NW == 8;  // (two waves of a work-group per SIMD)
   constexpr int DIST = PP ? 1 : 2;  // prefetch distance in blocks
   const bool late = PP && wave >= NW / 2;
   // barrier of block k: every own load but those of block k+DIST has landed (lockstep:
