@@ -20,12 +20,16 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-// XOR swizzle of 16-byte chunks within an LDS row: conflict-free both for the
-// 16 consecutive rows of a b128 score-operand read and for the 4-row x 4-chunk
-// footprint of a transposed read.
+// XOR swizzle of the 16-byte chunks within an LDS row (D / 8 chunks per row):
+// conflict-free both for the 16 consecutive rows of a b128 score-operand read (16 lanes
+// per pass over the 64 banks) and for the 4-row x 4-chunk footprint of a transposed read.
+// It depends on row bits 0..3 only, and not on bit 4, so the offsets of rows r and r + 16
+// differ by a constant (the transposed reads of both k steps share one base).
 template <int D>
 __device__ __forceinline__ int swz(int row) {
-  return (((row & 3) << 2) | ((row >> 2) & 3)) & (D / 8 - 1);  // D / 8 chunks per row
+  static_assert(D == 64 || D == 128, "head_dim 64 or 128");
+  if constexpr (D == 128) return ((row & 3) << 2) | ((row >> 2) & 3);
+  else return (((row >> 1) & 1) << 2) | ((row >> 2) & 3);  // 128-byte rows: two per 64 banks
 }
 
 template <int D>
