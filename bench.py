@@ -204,8 +204,8 @@ def main():
                     help="first run one plain device copy of this many MiB (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the kernel runs on one "
-              "GPU's share of heads and multi-GPU runs are not part of this build.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the kernels run on one "
+              "GPU's share of heads; a multi-GPU (head-sharded) run is not implemented.", file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
