@@ -63,6 +63,7 @@ SHAPES = [
     custom_workload("bwd_tf_f32_d128", 1, 2, 128, "f32", MASK_TEACHER_FORCING, 3, 20),
     custom_workload("bwd_tf_ragged_bf16", 2, 2, 128, "bf16", MASK_TEACHER_FORCING, 3, 100, tangent_std=0.5),
     custom_workload("bwd_tf_several_tiles_bf16", 1, 3, 128, "bf16", MASK_TEACHER_FORCING, 4, 300, tangent_std=0.5),
+    custom_workload("bwd_tf_five_heads_bf16", 1, 5, 128, "bf16", MASK_TEACHER_FORCING, 3, 150, tangent_std=0.5),
     custom_workload("bwd_tf_one_token_chunks_bf16", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, 64, 1,
                     tangent_std=0.5),
     custom_workload("bwd_tf_one_chunk_bf16", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, 1, 300, tangent_std=0.5),

@@ -64,6 +64,9 @@ def _check_full(w, seed=0):
 EDGE = [
     custom_workload("tf_ragged_bf16", 2, 2, 128, "bf16", MASK_TEACHER_FORCING, 3, 100, tangent_std=0.5),
     custom_workload("tf_several_tiles_bf16", 1, 3, 128, "bf16", MASK_TEACHER_FORCING, 4, 300, tangent_std=0.5),
+    # 3 x 3 = 9 (batch, head) pairs: two full groups of four heads and a group of one in the
+    # work-group order
+    custom_workload("tf_nine_heads_bf16", 3, 3, 128, "bf16", MASK_TEACHER_FORCING, 2, 170, tangent_std=0.5),
     custom_workload("tf_one_token_chunks_bf16", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, 64, 1, tangent_std=0.5),
     custom_workload("tf_one_chunk_bf16", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, 1, 300, tangent_std=0.5),
     custom_workload("tf_nonuniform_bf16", 1, 2, 128, "bf16", MASK_TEACHER_FORCING,

@@ -61,6 +61,7 @@ def _padded(x):
 SHAPES = [
     custom_workload("zc_ragged_bf16", 2, 2, 128, "bf16", MASK_TEACHER_FORCING, 3, 100, tangent_std=0.5),
     custom_workload("zc_several_tiles_bf16", 1, 3, 128, "bf16", MASK_TEACHER_FORCING, 4, 300, tangent_std=0.5),
+    custom_workload("zc_six_heads_bf16", 2, 3, 128, "bf16", MASK_TEACHER_FORCING, 3, 150, tangent_std=0.5),
     custom_workload("zc_tile_aligned_bf16", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, 4, 128, tangent_std=0.5),
     custom_workload("zc_one_token_chunks_bf16", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, 64, 1, tangent_std=0.5),
     custom_workload("zc_one_chunk_bf16", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, 1, 300, tangent_std=0.5),
