@@ -11,8 +11,11 @@
 //    plan) and accumulates gQ^T = K^T gS^T;
 //  - key-tile pass: a work-group owns 128 keys (4 waves x 32) and two halves of each
 //    64-row query block (waves 0..3 the first 32 rows, 4..7 the second), streams the
-//    query blocks that see its keys (the plan of the transposed, key-group table) and
+//    query blocks that see its keys (the plan of the transposed, key-group table)
+//    through a three-stage LDS ring (block it+2 loads while block it is used), and
 //    accumulates gV^T = gO^T P and gK^T = Q^T gS; the two halves are summed at the end.
+//    Each wave keeps the K operands of its 32 keys in registers (read once from LDS), so
+//    the LDS holds only the V tile and the three stages.
 // Matrix-core work: 6 D flop per (query, key) pair in the first pass, 8 D in the second
 // (the scores S and gP are computed in both), against 10 D for a single pass that would
 // need atomic gQ updates.
@@ -272,7 +275,7 @@ struct KGeo {
   static constexpr int KTB = KT * ROWB;         // K (or V) rows of the work-group's keys
   static constexpr int QTB = QB * ROWB;         // Q (or gO) rows of one query block
   static constexpr int SB = 2 * QTB + 2 * 4 * QB;  // stage: Q, gO, LSE, Delta of a block
-  static constexpr int BYTES = 2 * KTB + 2 * SB;
+  static constexpr int BYTES = KTB + 3 * SB;    // V tile, three query-block stages
   static constexpr int DT = D / 32;
   static constexpr int KS = D / 16;
   static constexpr int IPK = KTB / 1024;        // 1 KiB direct loads per key tile
@@ -286,8 +289,7 @@ __global__ __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(2, 2))
 void attn_bwd_dkdv_kernel(const BwdArgs a) {
   using G = KGeo<D>;
   __shared__ __attribute__((aligned(1024))) char lds[G::BYTES];
-  char* const sK = lds;
-  char* const stages = lds + 2 * G::KTB;
+  char* const stages = lds + G::KTB;  // the K tile passes through stages 1-2 at the start
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -356,7 +358,7 @@ void attn_bwd_dkdv_kernel(const BwdArgs a) {
   const int qoff = qh * 32 * G::ROWB;  // this wave's 32 rows within a query block tile
   // chunk 2s + hh of a row sits at the row's chunk-hh offset ^ (32 s)
   const unsigned qaoff = qoff + lds_off<D>(lane & 31, hh);
-  const unsigned kboff = lds_addr(sK) + lds_off<D>(krow, hh);
+  const unsigned kboff = lds_off<D>(krow, hh);
 
   f32x16 gk[G::DT], gv[G::DT];
 #pragma unroll
@@ -367,38 +369,57 @@ void attn_bwd_dkdv_kernel(const BwdArgs a) {
   const float c2 = a.scale * kLog2e;
 
   const unsigned lds_base = __builtin_amdgcn_readfirstlane(lds_addr(lds));
-  const unsigned st_lds = lds_base + 2 * G::KTB;
-  dma_rows(Kg, k0, lds_base, IC<G::IPK>{});
-  dma_rows(Vg, k0, lds_base + G::KTB, IC<G::IPK>{});
-  if (nblk > 0) dma_qblock(plan_block(plan, 0), st_lds);
+  const unsigned st_lds = lds_base + G::KTB;
+  // K tile into the space of stages 1-2, V tile to its own place; each wave then keeps the
+  // K operands of its 32 keys in registers for the whole kernel
+  const unsigned k_lds = st_lds + G::SB;
+  dma_rows(Kg, k0, k_lds, IC<G::IPK>{});
+  dma_rows(Vg, k0, lds_base, IC<G::IPK>{});
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
+  bf16x8 kreg[G::KS];
+#pragma unroll
+  for (int s = 0; s < G::KS; ++s) kreg[s] = ld128_at((k_lds + kboff) ^ (32u * s));
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (nblk > 0) {
+    dma_qblock(plan_block(plan, 0), st_lds);
+    dma_qblock(plan_block(plan, min(1, nblk - 1)), st_lds + G::SB);
+  }
+  __builtin_amdgcn_s_waitcnt(0xF70);
+  __syncthreads();
+  // loads per wave and block: the Q and gO rows, plus LSE (wave NW-2) or Delta (NW-1)
+  constexpr int LPB = 2 * ((G::IPQ + NW - 1) / NW);
+  static_assert(LPB == 4 || LPB == 2, "vmcnt immediates below");
+  const bool stat_wave = wave >= NW - 2;
+  int cur = 0;
 
   for (int it = 0; it < nblk; ++it) {
-    const char* cs = stages + (it & 1) * G::SB;
-    // the other stage was last read in iteration it-1, before the barrier that ended it
-    if (it + 1 < nblk) dma_qblock(plan_block(plan, it + 1), st_lds + (unsigned)(((it + 1) & 1) * G::SB));
+    const char* cs = stages + cur * G::SB;
+    // block it+2 into the stage of block it-1, last read before the barrier that ended
+    // iteration it-1 (past the end: the last block again, never read)
+    const int nx2 = cur == 0 ? 2 : cur - 1;
+    dma_qblock(plan_block(plan, min(it + 2, nblk - 1)), st_lds + (unsigned)(nx2 * G::SB));
     const int q0b = plan_block(plan, it) * QB;
 
     // S = Q K^T and gP = gO V^T (lane: key l%32, rows 8 (i/4) + 4 (l/32) + i%4 of the
     // half); operand reads one k step ahead of their MFMAs (order pinned with fences)
     f32x16 S = f32x16{}, GP = f32x16{};
     const unsigned qa = vreg_add(lds_addr(cs), qaoff);
-    const unsigned kb = vreg_add(0u, kboff, it);
-    bf16x8 aq[2], ag[2], bk[2], bv[2];
+    const unsigned kb = vreg_add(lds_base, kboff, it);
+    bf16x8 aq[2], ag[2], bv[2];
     auto read = [&](int s) {
       const unsigned x = 32u * s;
       aq[s & 1] = ld128_at(qa ^ x);
       ag[s & 1] = ld128_at((qa ^ x) + G::QTB);
-      bk[s & 1] = ld128_at(kb ^ x);
-      bv[s & 1] = ld128_at((kb ^ x) + G::KTB);
+      bv[s & 1] = ld128_at(kb ^ x);
     };
     read(0);
 #pragma unroll
     for (int s = 0; s < G::KS; ++s) {
       if (s + 1 < G::KS) read(s + 1);
       __builtin_amdgcn_sched_barrier(0);
-      S = mfma(aq[s & 1], bk[s & 1], S);
+      S = mfma(aq[s & 1], kreg[s], S);
       GP = mfma(ag[s & 1], bv[s & 1], GP);
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -462,8 +483,18 @@ void attn_bwd_dkdv_kernel(const BwdArgs a) {
       gk[dt] = mfma(qt[g & 1], gsb[t], gk[dt]);
       __builtin_amdgcn_sched_barrier(0);
     }
-    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    // every load but this iteration's (block it+2) has landed
+    if constexpr (LPB == 4) {
+      if (stat_wave) asm volatile("s_waitcnt vmcnt(5) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      else asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    } else {
+      if (stat_wave) asm volatile("s_waitcnt vmcnt(3) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      else asm volatile("s_waitcnt vmcnt(2) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    }
+    cur = cur == 2 ? 0 : cur + 1;
   }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // (the clamped tail loads)
+  __syncthreads();
 
   // Sum the two row halves: waves 4..7 leave their partial gK^T, gV^T in LDS (every
   // stage is idle after the last barrier), waves 0..3 add them and store.
