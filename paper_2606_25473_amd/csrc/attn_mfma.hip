@@ -80,6 +80,10 @@ template <bool B>
 struct Tag {
   static constexpr bool value = B;
 };
+template <int N>
+struct IC {
+  static constexpr int value = N;
+};
 
 // One work-group's query tile `qtile` of (batch, head) `bh`.  `stages` and `sdQ`
 // are the work-group's LDS buffers (sized for the JVP bodies).
@@ -238,6 +242,21 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   const float sc = a.scale;
   const int krow = lane & 31;
   const unsigned koff = lds_off<D>(krow, hh), dqoff = lds_off<D>(qrow, hh);
+  // The 4-wave forward kernel runs its block loop unrolled over the three stages: stage
+  // bases become instruction immediates and the per-step offsets stay in 16 registers, so
+  // its LDS reads need no address arithmetic (the 8-wave kernels have no registers to spare
+  // and form each offset with one XOR per step).
+  constexpr bool STATIC = MODE == kFwd && NW == 4;
+  unsigned koffs[STATIC ? G::KS : 1], vtro[2][STATIC ? G::DT : 1];
+  if constexpr (STATIC) {
+#pragma unroll
+    for (int s = 0; s < G::KS; ++s) koffs[s] = koff ^ (32u * s);
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt) {
+      vtro[0][dt] = trx0 ^ (64u * dt);
+      vtro[1][dt] = trx1 ^ (64u * dt);
+    }
+  }
 
   // Two schedules of the key-block loop, both with three LDS stages.
   //
@@ -275,17 +294,26 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   // group of MFMAs at a time, its operands read OPF groups ahead (the order is pinned with
   // scheduling fences: left to itself the compiler waits on each read right before its
   // MFMA)
-  auto ophase = [&](auto tk, const char* cV, const char* cdV, const bf16x8* pb, const bf16x8* hb) {
+  auto ophase = [&](auto tk, auto am, const char* cV, const char* cdV, const bf16x8* pb, const bf16x8* hb) {
     constexpr bool TK = JVP && decltype(tk)::value;
+    constexpr int C = decltype(am)::value;  // stage index known at compile time, or -1
     constexpr int OPF = JVP ? 1 : 2;
     constexpr int NG = 2 * G::DT;
-    const unsigned vb0 = vreg_add(lds_addr(cV), trx0), vb1 = vreg_add(lds_addr(cV), trx1);
+    const unsigned vb0 = C >= 0 ? 0u : vreg_add(lds_addr(cV), trx0);
+    const unsigned vb1 = C >= 0 ? 0u : vreg_add(lds_addr(cV), trx1);
     const unsigned dvo = (unsigned)(cdV - cV);
     bf16x8 vop[OPF + 1], dvop[OPF + 1];
     auto read = [&](int g) {
       const int t = g / G::DT, dt = g % G::DT, b = g % (OPF + 1);
       const unsigned o = 16u * t * G::ROWB;
-      const unsigned a0 = vb0 ^ (64u * dt), a1 = vb1 ^ (64u * dt);
+      unsigned a0, a1;
+      if constexpr (C >= 0) {
+        a0 = lds_addr(stages) + (unsigned)(C * SB + TB) + vtro[0][dt];
+        a1 = lds_addr(stages) + (unsigned)(C * SB + TB) + vtro[1][dt];
+      } else {
+        a0 = vb0 ^ (64u * dt);
+        a1 = vb1 ^ (64u * dt);
+      }
       vop[b] = cat(ld_tr_at(a0 + o), ld_tr_at(a1 + o));
       if constexpr (TK) dvop[b] = cat(ld_tr_at(a0 + o + dvo), ld_tr_at(a1 + o + dvo));
     };
@@ -306,9 +334,10 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   // One key block; TK: the block has tangent keys (dK, dV tiles are present).  Returns
   // true -- before touching any accumulator -- if some row's block max exceeds its
   // reference by more than kLazy; the caller then rescales and redoes the block.
-  auto step = [&](auto tk, int it, const char* cK, const char* cV, const char* cdK, const char* cdV,
+  auto step = [&](auto tk, auto am, int it, const char* cK, const char* cV, const char* cdK, const char* cdV,
                   unsigned next_stage) -> bool {
     constexpr bool TK = JVP && decltype(tk)::value;
+    constexpr int C = decltype(am)::value;  // stage index known at compile time, or -1
     // prefetch block it+DIST (redone, with the same data, when the block is redone).
     // Lockstep: a fixed number of loads per iteration, indices past the end clamped (that
     // stage is never read).
@@ -326,13 +355,14 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
     // with scheduling fences, as in the output phase); the dQ base is recomputed per
     // iteration (vreg_add with the iteration as a dependency) like the stage-relative ones
     constexpr int SPF = JVP ? 1 : 2;
-    const unsigned kb = vreg_add(lds_addr(cK), koff);
-    const unsigned dqb = vreg_add(lds_addr(sdQ), dqoff, it);
+    const unsigned kb = C >= 0 ? 0u : vreg_add(lds_addr(cK), koff);
+    const unsigned dqb = JVP ? vreg_add(lds_addr(sdQ), dqoff, it) : 0u;
     const unsigned dko = (unsigned)(cdK - cK);
     bf16x8 kop[SPF + 1], dkop[SPF + 1], dqop[SPF + 1];
     auto read = [&](int s) {
       const int b = s % (SPF + 1);
-      kop[b] = ld128_at(kb ^ (32u * s));
+      if constexpr (C >= 0) kop[b] = ld128_at(lds_addr(stages) + (unsigned)(C * SB) + koffs[s]);
+      else kop[b] = ld128_at(kb ^ (32u * s));
       if constexpr (TK) dkop[b] = ld128_at((kb ^ (32u * s)) + dko);
       if constexpr (JVP) dqop[b] = ld128_at(dqb ^ (32u * s));
     };
@@ -399,7 +429,7 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
 
     if constexpr (PP) __builtin_amdgcn_s_setprio(0);
     if (late) end_iteration();
-    ophase(tk, cV, cdV, pb, hb);
+    ophase(tk, am, cV, cdV, pb, hb);
     if (!late) end_iteration();
     return false;
   };
@@ -437,14 +467,41 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
       while (it < ntk) {
         const int nxt = PP ? (cur == 2 ? 0 : cur + 1) : (cur == 0 ? 2 : cur - 1);  // (it + DIST) mod 3
         const char* cs = stages + cur * SB;
-        rescale = step(Tag<false>{}, it, cs, cs + TB, cs + 2 * TB, cs + 2 * TB + TBJ,
+        rescale = step(Tag<false>{}, IC<-1>{}, it, cs, cs + TB, cs + 2 * TB, cs + 2 * TB + TBJ,
                        st_lds + (unsigned)(nxt * SB));
         if (rescale) break;
         ++it;
         cur = cur == 2 ? 0 : cur + 1;
       }
     }
-    if (!rescale) {
+    if constexpr (STATIC) {
+      // three copies of the step, one per stage: block it is in stage it mod 3, block it+2
+      // streams into stage (it+2) mod 3
+      auto sstep = [&](auto am) -> bool {
+        constexpr int C = decltype(am)::value;
+        char* cs = stages + C * SB;
+        return step(Tag<false>{}, am, it, cs, cs + TB, cs + 2 * TB, cs + 2 * TB + TBJ,
+                    st_lds + (unsigned)(((C + 2) % 3) * SB));
+      };
+      while (it < nblk) {
+        if (cur == 0) {
+          rescale = sstep(IC<0>{});
+          if (rescale) break;
+          cur = 1;
+          if (++it >= nblk) break;
+        }
+        if (cur == 1) {
+          rescale = sstep(IC<1>{});
+          if (rescale) break;
+          cur = 2;
+          if (++it >= nblk) break;
+        }
+        rescale = sstep(IC<2>{});
+        if (rescale) break;
+        cur = 0;
+        ++it;
+      }
+    } else if (!rescale) {
       while (it < nblk) {
         const int nxt = PP ? (cur == 2 ? 0 : cur + 1) : (cur == 0 ? 2 : cur - 1);  // (it + DIST) mod 3
         char* cs = stages + cur * SB;
@@ -459,7 +516,7 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
             cleared = it;
           }
         }
-        rescale = step(Tag<true>{}, it, cs, cs + TB, cs + 2 * TB, cs + 2 * TB + TBJ,
+        rescale = step(Tag<true>{}, IC<-1>{}, it, cs, cs + TB, cs + 2 * TB, cs + 2 * TB + TBJ,
                        st_lds + (unsigned)(nxt * SB));
         if (rescale) break;
         ++it;
