@@ -247,6 +247,12 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   // its LDS reads need no address arithmetic (the 8-wave kernels have no registers to spare
   // and form each offset with one XOR per step).
   constexpr bool STATIC = MODE == kFwd && NW == 4;
+  // (JVP) the dQ operand offsets do not depend on the stage: 8 registers, no arithmetic
+  unsigned dqoffs[JVP ? G::KS : 1];
+  if constexpr (JVP) {
+#pragma unroll
+    for (int s = 0; s < G::KS; ++s) dqoffs[s] = lds_addr(sdQ) + (dqoff ^ (32u * s));
+  }
   unsigned koffs[STATIC ? G::KS : 1], vtro[2][STATIC ? G::DT : 1];
   if constexpr (STATIC) {
 #pragma unroll
@@ -352,11 +358,9 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
     if constexpr (PP) __builtin_amdgcn_s_setprio(1);
     f32x16 S = f32x16{}, dS = f32x16{};
     // operand reads run SPF k steps ahead of the MFMAs that consume them (order pinned
-    // with scheduling fences, as in the output phase); the dQ base is recomputed per
-    // iteration (vreg_add with the iteration as a dependency) like the stage-relative ones
+    // with scheduling fences, as in the output phase)
     constexpr int SPF = JVP ? 1 : 2;
     const unsigned kb = C >= 0 ? 0u : vreg_add(lds_addr(cK), koff);
-    const unsigned dqb = JVP ? vreg_add(lds_addr(sdQ), dqoff, it) : 0u;
     const unsigned dko = (unsigned)(cdK - cK);
     bf16x8 kop[SPF + 1], dkop[SPF + 1], dqop[SPF + 1];
     auto read = [&](int s) {
@@ -364,7 +368,7 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
       if constexpr (C >= 0) kop[b] = ld128_at(lds_addr(stages) + (unsigned)(C * SB) + koffs[s]);
       else kop[b] = ld128_at(kb ^ (32u * s));
       if constexpr (TK) dkop[b] = ld128_at((kb ^ (32u * s)) + dko);
-      if constexpr (JVP) dqop[b] = ld128_at(dqb ^ (32u * s));
+      if constexpr (JVP) dqop[b] = ld128_at(dqoffs[s]);
     };
 #pragma unroll
     for (int s = 0; s < SPF; ++s) read(s);
