@@ -402,10 +402,7 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
     }
 
     // ---- online softmax.  The scale is positive, so max(S) * c2 = max(S * c2).
-    float mxr = sv[0];
-#pragma unroll
-    for (int i = 1; i < 16; ++i) mxr = fmaxf(mxr, sv[i]);
-    const float mloc = mxr * c2;
+    const float mloc = max16(sv) * c2;
     if (__ballot(mloc > m + kLazy) != 0) {
       mpend = mloc;
       return true;
