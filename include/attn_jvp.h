@@ -29,6 +29,10 @@
  *   keeps no per-call state, so calls are reentrant and may be captured in a
  *   HIP graph.  Inputs are never written.  Outputs must not overlap inputs or
  *   each other (checked by address range; overlap is ATTN_ERR_INVALID).
+ * - Sizes: B, H, L >= 1, B * H <= 2^20; bf16 inputs need L * D <= 2^31 (the kernels
+ *   address a head with 32-bit byte offsets) and ceil(L / 128) * B * H <= 2^31 - 1
+ *   (work-groups of one launch); fp32 inputs need B * H <= 65535 (one grid row per
+ *   (batch, head)).  Larger sizes are ATTN_ERR_INVALID.
  * - Return codes: ATTN_OK, or ATTN_ERR_INVALID (bad pointer, size or layout),
  *   ATTN_ERR_UNSUPPORTED (dtype / head_dim not built), ATTN_ERR_HIP (a HIP
  *   launch error).  All argument and layout validation happens before any HIP

@@ -28,6 +28,25 @@ struct Span {
 
 bool overlap(const Span& x, const Span& y) { return x.lo < y.hi && y.lo < x.hi; }
 
+// Size limits of the kernels (after the positivity checks): the bf16 kernels address a
+// head with 32-bit byte offsets and launch one work-group per tile of at least 128 rows
+// or keys and (batch, head) along x; the fp32 kernels launch one grid row per (batch,
+// head) along y.
+int check_sizes(int dtype, int B, int H, int L, int D) {
+  const int64_t bh = (int64_t)B * H;
+  if (bh > (int64_t)1 << 20) return fail(ATTN_ERR_INVALID, "B * H too large");
+  if (dtype == ATTN_DTYPE_BF16) {
+    if ((int64_t)L * D > (int64_t)1 << 31)
+      return fail(ATTN_ERR_INVALID, "bf16 needs L * D <= 2^31 (32-bit offsets within a head), got L = " +
+                                        std::to_string(L) + ", D = " + std::to_string(D));
+    if (((int64_t)L + 127) / 128 * bh > INT32_MAX)
+      return fail(ATTN_ERR_INVALID, "too many work-groups for one launch: ceil(L / 128) * B * H > 2^31 - 1");
+  } else if (bh > 65535) {
+    return fail(ATTN_ERR_INVALID, "fp32 needs B * H <= 65535, got " + std::to_string(bh));
+  }
+  return ATTN_OK;
+}
+
 int elem_size(int dtype) { return dtype == ATTN_DTYPE_F32 ? 4 : dtype == ATTN_DTYPE_BF16 ? 2 : 0; }
 
 // Shared validation of the compute entry points; fills the launch arguments.
@@ -46,7 +65,7 @@ int prepare(attn::Pass pass, int dtype, int B, int H, int L, int D, const void* 
   if (B <= 0 || H <= 0 || L <= 0)
     return fail(ATTN_ERR_INVALID, "B, H and L must be positive (B=" + std::to_string(B) +
                                       ", H=" + std::to_string(H) + ", L=" + std::to_string(L) + ")");
-  if ((int64_t)B * H > (int64_t)1 << 20) return fail(ATTN_ERR_INVALID, "B * H too large");
+  if (const int rc = check_sizes(dtype, B, H, L, D)) return rc;
   if (!Q || !K || !V || !O || !LSE) return fail(ATTN_ERR_INVALID, "NULL tensor pointer");
   if (jvp && (!dQ || !dK || !dV || !dO)) return fail(ATTN_ERR_INVALID, "NULL tangent pointer");
   if (!layout) return fail(ATTN_ERR_INVALID, "layout is NULL");
@@ -115,7 +134,7 @@ int prepare_bwd(int dtype, int B, int H, int L, int D, const void* Q, const void
   if (B <= 0 || H <= 0 || L <= 0)
     return fail(ATTN_ERR_INVALID, "B, H and L must be positive (B=" + std::to_string(B) +
                                       ", H=" + std::to_string(H) + ", L=" + std::to_string(L) + ")");
-  if ((int64_t)B * H > (int64_t)1 << 20) return fail(ATTN_ERR_INVALID, "B * H too large");
+  if (const int rc = check_sizes(dtype, B, H, L, D)) return rc;
   const void* ins[6] = {Q, K, V, O, gO, LSE};
   const char* in_names[6] = {"Q", "K", "V", "O", "gO", "LSE"};
   void* outs[4] = {gQ, gK, gV, Delta};

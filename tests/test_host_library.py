@@ -261,6 +261,12 @@ def _call(lib, **kw):
     (dict(layout=make_layout("ranges", [(30, 0, 10, 0, 0), (30, 0, 64, 0, 0)])), 1, "increasing"),
     (dict(layout=make_layout("ranges", [(64, 0, 65, 0, 0)])), 1, "begin <= end <= L"),
     (dict(layout=make_layout("ranges", [])), 1, "query groups"),
+    # size limits: 32-bit offsets within a bf16 head, work-groups per launch, fp32 grid rows
+    (dict(L=(1 << 24) + 2, D=128, layout=make_layout("teacher_forcing", [0, (1 << 23) + 1])), 1, "2^31"),
+    (dict(L=(1 << 25) + 2, D=64, layout=make_layout("teacher_forcing", [0, (1 << 24) + 1])), 1, "2^31"),
+    (dict(B=1024, H=1024, L=1 << 18, D=64), 1, "work-groups"),
+    (dict(B=2, H=1 << 20), 1, "B * H too large"),
+    (dict(dtype=0, B=256, H=256, L=16), 1, "65535"),
 ])
 @_no_gpu
 def test_invalid_arguments_are_rejected_before_any_hip_call(lib, kw, code, needle):
@@ -311,6 +317,18 @@ def test_backward_entry_point_validates(lib):
     assert call(p, D=80) == 2 and "head_dim" in binding.last_error()
     three = [(8, 0, 1, 0, 0), (16, 1, 2, 0, 0), (24, 0, 1, 0, 0), (32, 1, 2, 0, 0), (64, 0, 1, 0, 0)]
     assert call(p, layout=make_layout("ranges", three)) == 2 and "two query ranges" in binding.last_error()
+
+
+@_no_gpu
+def test_largest_accepted_sizes_pass_the_size_checks(lib):
+    # the largest bf16 head (L * D = 2^31) and an fp32 launch of 65535 (batch, head) pairs pass
+    # the size checks: the first failure is then a deliberately bad layout (checked later)
+    bad = make_layout("teacher_forcing", [0, 16, 40])
+    assert _call(lib, L=1 << 24, D=128, layout=bad) == 1 and "L = 2" in binding.last_error()
+    assert _call(lib, dtype=0, B=65535, H=1, L=16, layout=bad) == 1 and "L = 2" in binding.last_error()
+    p = _ptrs(10, 2, 1, 1, 1 << 24, 128)
+    rc = lib.attn_bwd(1, 1, 1, (1 << 24) + 2, 128, *p[:6], ctypes.byref(make_layout("full")), 0.0, *p[6:], None)
+    assert rc == 1 and "2^31" in binding.last_error()
 
 
 @_no_gpu
