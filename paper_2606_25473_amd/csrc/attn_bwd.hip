@@ -34,6 +34,11 @@ namespace {
 
 using namespace dev;
 
+template <int N>
+struct IC {  // a compile-time count (or stage index) passed to a generic lambda
+  static constexpr int value = N;
+};
+
 constexpr int NW = 8;  // waves per work-group in both bf16 passes
 constexpr int NTHREADS = 64 * NW;
 
@@ -138,28 +143,47 @@ void attn_bwd_dq_kernel(const BwdArgs a) {
   for (int dt = 0; dt < G::DT; ++dt) gacc[dt] = f32x16{};
   const float c2 = a.scale * kLog2e;
   const int krow = lane & 31;
-  const unsigned koff = lds_off<D>(krow, hh);  // chunk 2s + hh of the row: koff ^ (32 s)
+  // Per-lane LDS offsets of the operand reads within a stage, kept in 16 registers: chunk
+  // 2s + hh of the lane's key row (K and V reads of k step s) and the transposed K reads of
+  // key half p and d tile dt.  The block loop is unrolled over the three stages, so the
+  // stage base is an instruction immediate and the reads need no address arithmetic.
+  const unsigned koff = lds_off<D>(krow, hh);
+  unsigned koffs[G::KS], ktro[2][G::DT];
+#pragma unroll
+  for (int s = 0; s < G::KS; ++s) koffs[s] = koff ^ (32u * s);
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt) {
+    ktro[0][dt] = trx[0] ^ (64u * dt);
+    ktro[1][dt] = trx[1] ^ (64u * dt);
+  }
 
   // wait for every load but this iteration's prefetch (2 per wave at D = 128; at D = 64
   // waves 0..3 issue one per tile and the others none), then synchronise
   auto end_iteration = []() { asm volatile("s_waitcnt vmcnt(2) lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
   static_assert((G::IPT + NW - 1) / NW == 1, "one direct load per tile and wave");
 
-  auto step = [&](int it, const char* cK, const char* cV, unsigned next_stage) {
-    dma_block(plan_block(plan, min(it + 2, nblk - 1)), next_stage);
+  // block it is in stage C = it mod 3; block it+2 streams into stage (C + 2) mod 3
+  auto step = [&](auto am, int it) {
+    constexpr int C = decltype(am)::value;
+    // (opaque to the compiler: otherwise it hoists offset + stage base out of the loop, one
+    // register per offset and stage, instead of folding the base into each read's immediate)
+#pragma unroll
+    for (int s = 0; s < G::KS; ++s) asm volatile("" : "+v"(koffs[s]));
+#pragma unroll
+    for (int dt = 0; dt < G::DT; ++dt) asm volatile("" : "+v"(ktro[0][dt]), "+v"(ktro[1][dt]));
+    const unsigned sbase = lds_addr(stages) + (unsigned)(C * SB);  // (a compile-time constant)
+    dma_block(plan_block(plan, min(it + 2, nblk - 1)), lds_addr(stages) + (unsigned)(((C + 2) % 3) * SB));
     const int k0 = plan_block(plan, it) * QBC;
     // S^T = K Q^T and gP^T = V gO^T (lane: query l%32, keys 8 (i/4) + 4 (l/32) + i%4);
     // operand reads run SPF k steps ahead of their MFMAs (order pinned with scheduling
     // fences)
     f32x16 S = f32x16{}, GP = f32x16{};
     constexpr int SPF = 2;
-    const unsigned kb = vreg_add(lds_addr(cK), koff);
-    const unsigned vo = (unsigned)(cV - cK);
     bf16x8 kop[SPF + 1], vop[SPF + 1];
     auto read = [&](int s) {
       const int b = s % (SPF + 1);
-      kop[b] = ld128_at(kb ^ (32u * s));
-      vop[b] = ld128_at((kb ^ (32u * s)) + vo);
+      kop[b] = ld128_at(sbase + koffs[s]);
+      vop[b] = ld128_at(sbase + TB + koffs[s]);
     };
 #pragma unroll
     for (int s = 0; s < SPF; ++s) read(s);
@@ -195,12 +219,11 @@ void attn_bwd_dq_kernel(const BwdArgs a) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) gsb[t][j] = (bf16_t)gs[8 * t + j];
     constexpr int OPF = 2, NG = 2 * G::DT;
-    const unsigned tb0 = vreg_add(lds_addr(cK), trx[0]), tb1 = vreg_add(lds_addr(cK), trx[1]);
     bf16x8 kt[OPF + 1];
     auto read_t = [&](int g) {
       const int t = g / G::DT, dt = g % G::DT;
-      const unsigned o = 16u * t * G::ROWB;
-      kt[g % (OPF + 1)] = cat(ld_tr_at((tb0 ^ (64u * dt)) + o), ld_tr_at((tb1 ^ (64u * dt)) + o));
+      const unsigned o = sbase + 16u * t * G::ROWB;
+      kt[g % (OPF + 1)] = cat(ld_tr_at(o + ktro[0][dt]), ld_tr_at(o + ktro[1][dt]));
     };
 #pragma unroll
     for (int g = 0; g < OPF; ++g) read_t(g);
@@ -221,13 +244,16 @@ void attn_bwd_dq_kernel(const BwdArgs a) {
   }
   __builtin_amdgcn_s_waitcnt(0xF70);  // (builtin: also retires the operand loads above)
   __syncthreads();
-  int cur = 0;
-  for (int it = 0; it < nblk; ++it) {
-    const int nxt = cur == 0 ? 2 : cur - 1;  // (it + 2) mod 3
-    const char* cs = stages + cur * SB;
-    step(it, cs, cs + TB, st_lds + (unsigned)(nxt * SB));
-    cur = cur == 2 ? 0 : cur + 1;
+  // (whole triples in a loop without early exits, then the remainder: written with an exit
+  // after each step, the three copies made the register allocator spill)
+  int it = 0;
+  for (; it + 3 <= nblk; it += 3) {
+    step(IC<0>{}, it);
+    step(IC<1>{}, it + 1);
+    step(IC<2>{}, it + 2);
   }
+  if (it < nblk) step(IC<0>{}, it);
+  if (it + 1 < nblk) step(IC<1>{}, it + 1);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the clamped tail prefetches
 
   if (row < L) {
@@ -248,10 +274,6 @@ void attn_bwd_dq_kernel(const BwdArgs a) {
 
 constexpr int KT = kBwdKeysPerTile;   // 128 keys per work-group (4 key groups of 32)
 
-template <int N>
-struct IC {  // a compile-time count passed to a generic lambda
-  static constexpr int value = N;
-};
 constexpr int QB = kBwdRowsPerBlock;  // 64 query rows per block (2 halves of 32)
 
 // Direct global -> LDS load of 4 bytes per lane (lane l's bytes land at lds + 4 l);
