@@ -585,7 +585,7 @@ void attn_mfma_kernel(const AttnArgs a) {
   // LDS: three stages of K, V (+ dK, dV) tiles, and (JVP) the dQ tile of the query
   // tile, read back as an MFMA operand (keeps the per-wave register footprint within
   // two waves per SIMD).  D = 128 JVP: 3 x 32 KiB + 64 KiB = 160 KiB.
-  constexpr int SB = JVP ? 4 * G::TILEB : 2 * G::TILEB + 32;
+  constexpr int SB = JVP ? 4 * G::TILEB : 2 * G::TILEB;  // (the stage size tile_body uses)
   __shared__ __attribute__((aligned(1024))) char stages[3 * SB];
   __shared__ __attribute__((aligned(1024))) char sdQ[JVP ? 32 * NW * G::ROWB : 16];
 
