@@ -316,12 +316,18 @@ def main():
         "unmasked_pairs_per_head": pairs,
         "computed_over_unmasked": round(computed / pairs, 4),
     }
-    if prof.get("clock_ghz"):
-        # the nominal peak assumes 2.4 GHz; under this load the shader clock is lower
-        clk = prof["clock_ghz"]
-        res["roofline"]["measured_clock_ghz"] = round(clk, 3)
-        res["roofline"]["frac_at_measured_clock"] = round(achieved / (peak * clk / 2.4), 4)
-        res["roofline"]["mfma_busy_cycles_frac"] = round(prof.get("mfma_busy", 0.0), 4)
+    if prof.get("clock_ghz") and prof.get("trace_kernel_ms"):
+        # The committed profile run of this kernel source (possibly on another box, whose shader
+        # clock under this load may differ): its mean launch time, its clock (the nominal peak
+        # assumes 2.4 GHz) and its matrix-core busy fraction, and the roofline fraction at that
+        # clock from that run's own launch time.
+        clk, pms = prof["clock_ghz"], prof["trace_kernel_ms"]
+        if mode == "bwd":  # a call is two launches: add the query-tile pass's time
+            pms += profile_record(w.name, "bwd_dq").get("trace_kernel_ms", float("nan"))
+        res["roofline"]["profile"] = {
+            "kernel_ms": round(pms, 4), "clock_ghz": round(clk, 3),
+            "frac_at_clock": round(flop / (pms * 1e-3) / 1e12 / (peak * clk / 2.4), 4),
+            "mfma_busy_cycles_frac": round(prof.get("mfma_busy", 0.0), 4)}
     if mode == "zc":
         # the dense JVP of the same function (tangents zero-padded over the clean half)
         pad = {n: torch.cat([torch.zeros_like(x[n + "n"]), x[n + "n"]], dim=2) for n in ("dQ", "dK", "dV")}

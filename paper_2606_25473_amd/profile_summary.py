@@ -76,8 +76,12 @@ def main(argv=None):
     ap.add_argument("--pmc", nargs="*", default=[], help="counter-collection output dirs to list")
     a = ap.parse_args(argv)
     lines = []
+    derived = {}
     if a.trace:
         st = sorted(kernel_stats(a.trace), key=lambda r: -r[2] * r[1])
+        mine = [r for r in st if attn_kernel_of(a.op)(r[0])]
+        if mine:
+            derived["trace_kernel_ms"] = mine[0][2] / 1e6  # mean launch time under the tracer
         lines.append("| kernel | calls | avg ms | min ms | max ms | % time |")
         lines.append("|---|---|---|---|---|---|")
         for name, calls, avg, mn, mx, pct in st[:8]:
@@ -105,7 +109,6 @@ def main(argv=None):
             traffic = out["read"] + out["write"]
             lines.append(f"HBM traffic per launch: {traffic / 1e9:.3f} GB "
                          f"(read {out['read'] / 1e9:.3f} + write {out['write'] / 1e9:.3f})")
-    derived = {}
     is_attn = attn_kernel_of(a.op)
     for d in a.pmc:
         per, dur = {}, []
