@@ -202,17 +202,19 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
       if (lw >= 0 && (G::IPT % NI == 0 || j < G::IPT)) dma_rows_t(src, k0, j * RPI, dst);
     }
   };
-  // the K, V (and dK, dV) tiles of key block kb into the stage at LDS address st.  The
-  // tangent tiles are streamed for every block, also for blocks below t0 whose step does
-  // not read them (they then hold tangent row 0): a block-dependent load count would
-  // split the step into more basic blocks and cost registers the kernel does not have.
+  // the K, V (and dK, dV) tiles of key block kb into the stage at LDS address st.  A
+  // zero-clean block wholly below t0 loads no tangent tiles (its step does not read them;
+  // the stage keeps an older block's).  The load count then depends on the block, which
+  // only the ping-pong schedule allows: it waits for all loads at each barrier.
   auto dma_block = [&](int kb, unsigned st) {
     const int k0 = kb * BC;
     dma_tile(Kg, k0, st);
     dma_tile(Vg, k0, st + TB);
     if constexpr (JVP) {
-      dma_tile_t(dKg, k0, st + 2 * TB);
-      dma_tile_t(dVg, k0, st + 2 * TB + TBJ);
+      if (!ZC || k0 + BC > t0) {
+        dma_tile_t(dKg, k0, st + 2 * TB);
+        dma_tile_t(dVg, k0, st + 2 * TB + TBJ);
+      }
     }
   };
   // clear the first nrows rows of an LDS tile (16 bytes per thread and pass)
@@ -289,6 +291,7 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   // its softmax overlaps the other wave's output MFMAs.
   constexpr bool PP = NW == 8;  // (two waves of a work-group per SIMD)
   constexpr int DIST = PP ? 1 : 2;  // prefetch distance in blocks
+  static_assert(!ZC || PP, "zero-clean load counts vary by block: only full waits are correct");
   const bool late = PP && wave >= NW / 2;
   // barrier of block k: every own load but those of block k+DIST has landed (lockstep:
   // N per wave; D = 128: one per tile and wave; D = 64: waves 0..3 issue one, the others
