@@ -70,7 +70,7 @@ void attn_bwd_dq_kernel(const BwdArgs a) {
   const int hh = lane >> 5;
   const int L = a.L;
 
-  const TileSlot sl = slot_of(blockIdx.x, a.B * a.H, a.order.nt);
+  const TileSlot sl = slot_of(blockIdx.x, a.B * a.H, a.order.nt, kHeadGroupWide);
   const int bh = sl.bh;
   const int qtile = tile_of(a.order, sl.pos);
   const size_t head = (size_t)bh * L * D;
@@ -321,7 +321,7 @@ void attn_bwd_dkdv_kernel(const BwdArgs a) {
   const int qh = wave >> 2;  // which 32 rows of each query block
   const int L = a.L;
 
-  const TileSlot sl = slot_of(blockIdx.x, a.B * a.H, a.order.nt);
+  const TileSlot sl = slot_of(blockIdx.x, a.B * a.H, a.order.nt, kHeadGroupWide);
   const int bh = sl.bh;
   const int ktile = tile_of(a.order, sl.pos);
   const size_t head = (size_t)bh * L * D;

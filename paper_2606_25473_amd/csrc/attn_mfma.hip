@@ -597,7 +597,7 @@ void attn_mfma_kernel(const AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) char stages[3 * SB];
   __shared__ __attribute__((aligned(1024))) char sdQ[JVP ? 32 * NW * G::ROWB : 16];
 
-  const TileSlot sl = slot_of(blockIdx.x, a.B * a.H, a.order.nt);
+  const TileSlot sl = slot_of(blockIdx.x, a.B * a.H, a.order.nt, MODE == kZeroClean ? kHeadGroupWide : kHeadGroup);
   const int bh = sl.bh;
   const int qtile = tile_of(a.order, sl.pos);
   if constexpr (MODE == kZeroClean) {

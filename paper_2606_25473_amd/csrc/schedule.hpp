@@ -167,25 +167,29 @@ ATTN_HD int tile_of(const TileOrder& o, int t) {
 }
 
 // Work-group b of a launch over nbh (batch, head) pairs and nt tiles per pair: the pairs
-// form groups of kHeadGroup, taken one group after another; inside a group, work-groups
-// go position-major (every pair's first tile of the order, then every pair's second, ...).
+// form groups of hg, taken one group after another; inside a group, work-groups go
+// position-major (every pair's first tile of the order, then every pair's second, ...).
 // So the heaviest tiles of a group's heads are dispatched first, before any light one,
 // and a run never ends on a few long tiles of the last head (heads one after another
-// leave such a tail); and only about kHeadGroup heads' keys and values are in flight at
-// once, which keeps the caches useful (all heads at once slowed launches over many heads).
-constexpr int kHeadGroup = 4;
+// leave such a tail); and only about hg heads' keys and values are in flight at once,
+// which keeps the caches useful (all heads at once slowed launches over many heads).
+// Work-group b runs on XCD b mod 8, so with hg = 4 or 8 each XCD works on one head.
+// Measured: groups of 4 for the JVP and forward kernels, 8 for the zero-clean JVP and
+// the backward passes.
+constexpr int kHeadGroup = 4;      // JVP, forward
+constexpr int kHeadGroupWide = 8;  // zero-clean JVP, backward
 
 struct TileSlot {
   int bh, pos;
 };
 
-ATTN_HD TileSlot slot_of(int b, int nbh, int nt) {
-  const int grp = b / (kHeadGroup * nt);
-  const int gsz = imin(kHeadGroup, nbh - grp * kHeadGroup);
-  const int r = b - grp * kHeadGroup * nt;
+ATTN_HD TileSlot slot_of(int b, int nbh, int nt, int hg) {
+  const int grp = b / (hg * nt);
+  const int gsz = imin(hg, nbh - grp * hg);
+  const int r = b - grp * hg * nt;
   TileSlot s;
   s.pos = r / gsz;
-  s.bh = grp * kHeadGroup + (r - s.pos * gsz);
+  s.bh = grp * hg + (r - s.pos * gsz);
   return s;
 }
 

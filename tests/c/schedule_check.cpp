@@ -10,19 +10,27 @@
 
 int main() {
   int fails = 0;
-  for (int nbh : {1, 2, 11, 12, 13, 24, 80}) {
-    for (int nt : {1, 7, 256, 1025}) {
-      std::set<std::pair<int, int>> seen;
-      for (int b = 0; b < nbh * nt; ++b) {
-        const attn::TileSlot s = attn::slot_of(b, nbh, nt);
-        if (s.bh < 0 || s.bh >= nbh || s.pos < 0 || s.pos >= nt) ++fails;
-        seen.insert({s.bh, s.pos});
+  for (int hg : {attn::kHeadGroup, attn::kHeadGroupWide}) {
+    for (int nbh : {1, 2, 11, 12, 13, 24, 80}) {
+      for (int nt : {1, 7, 256, 1025}) {
+        std::set<std::pair<int, int>> seen;
+        for (int b = 0; b < nbh * nt; ++b) {
+          const attn::TileSlot s = attn::slot_of(b, nbh, nt, hg);
+          if (s.bh < 0 || s.bh >= nbh || s.pos < 0 || s.pos >= nt) ++fails;
+          seen.insert({s.bh, s.pos});
+        }
+        if ((int)seen.size() != nbh * nt) { std::printf("slot_of hg=%d nbh=%d nt=%d\n", hg, nbh, nt); ++fails; }
+        // inside a group, position-major: the first group's first nbh' slots are position 0
+        const int g0 = nbh < hg ? nbh : hg;
+        for (int b = 0; b < g0; ++b)
+          if (attn::slot_of(b, nbh, nt, hg).pos != 0) { std::printf("position-major\n"); ++fails; break; }
+        // each XCD (work-group b mod 8) sees one head of the first group while it lasts
+        if (nbh >= hg && nt >= 8)
+          for (int b = 0; b + 8 < hg * nt; ++b)
+            if (attn::slot_of(b, nbh, nt, hg).bh != attn::slot_of(b + 8, nbh, nt, hg).bh) {
+              std::printf("one head per XCD hg=%d nbh=%d nt=%d\n", hg, nbh, nt); ++fails; break;
+            }
       }
-      if ((int)seen.size() != nbh * nt) { std::printf("slot_of nbh=%d nt=%d\n", nbh, nt); ++fails; }
-      // inside a group, position-major: the first group's first nbh' slots are position 0
-      const int g0 = nbh < attn::kHeadGroup ? nbh : attn::kHeadGroup;
-      for (int b = 0; b < g0; ++b)
-        if (attn::slot_of(b, nbh, nt).pos != 0) { std::printf("position-major\n"); ++fails; break; }
     }
   }
   for (int mode : {0, 1, 2}) {
