@@ -70,7 +70,7 @@ void attn_bwd_dq_kernel(const BwdArgs a) {
   const int hh = lane >> 5;
   const int L = a.L;
 
-  const TileSlot sl = slot_of(blockIdx.x, a.B * a.H, a.order.nt, kHeadGroupWide);
+  const TileSlot sl = slot_of(blockIdx.x, a.B * a.H, a.order.nt, kHeadGroup);
   const int bh = sl.bh;
   const int qtile = tile_of(a.order, sl.pos);
   const size_t head = (size_t)bh * L * D;

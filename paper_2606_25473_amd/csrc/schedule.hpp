@@ -174,10 +174,10 @@ ATTN_HD int tile_of(const TileOrder& o, int t) {
 // leave such a tail); and only about hg heads' keys and values are in flight at once,
 // which keeps the caches useful (all heads at once slowed launches over many heads).
 // Work-group b runs on XCD b mod 8, so with hg = 4 or 8 each XCD works on one head.
-// Measured: groups of 4 for the JVP and forward kernels, 8 for the zero-clean JVP and
-// the backward passes.
-constexpr int kHeadGroup = 4;      // JVP, forward
-constexpr int kHeadGroupWide = 8;  // zero-clean JVP, backward
+// Measured: groups of 4 for the JVP, forward and backward query-tile kernels, 8 for the
+// zero-clean JVP and the backward key-tile pass.
+constexpr int kHeadGroup = 4;      // JVP, forward, backward query-tile pass
+constexpr int kHeadGroupWide = 8;  // zero-clean JVP, backward key-tile pass
 
 struct TileSlot {
   int bh, pos;
