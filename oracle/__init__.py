@@ -9,7 +9,8 @@ Contents
 --------
 masks      -- the attention mask materialised from its definition (per-token
               chunk ids), for the full, block-causal and teacher-forcing kinds,
-              and from an explicit query-group / key-range list.
+              and from an explicit query-group / key-range list (any number
+              of key ranges per group).
 attention  -- closed-form masked attention O, LSE and the forward-mode tangent
               dO (paper, App. B, the masked-attention and tangent equations),
               and the same JVP with zero tangents on the clean half of a
@@ -24,12 +25,13 @@ Parity status: every function here is pinned by tests in
 scaled_dot_product_attention and torch.func.jvp, the two-pass TF identity,
 hand-derived golden values and invariants).
 """
-from .masks import MASK_FULL, MASK_BLOCK_CAUSAL, MASK_TEACHER_FORCING, MASK_RANGES, allowed_mask, count_allowed_pairs
+from .masks import (MASK_FULL, MASK_BLOCK_CAUSAL, MASK_TEACHER_FORCING, MASK_RANGES, allowed_mask, check_groups,
+                    count_allowed_pairs)
 from .attention import attention_jvp, attention_fwd, attention_jvp_zero_clean
 from .backward import attention_vjp
 
 __all__ = [
     "MASK_FULL", "MASK_BLOCK_CAUSAL", "MASK_TEACHER_FORCING", "MASK_RANGES",
-    "allowed_mask", "count_allowed_pairs", "attention_jvp", "attention_fwd", "attention_jvp_zero_clean",
+    "allowed_mask", "check_groups", "count_allowed_pairs", "attention_jvp", "attention_fwd", "attention_jvp_zero_clean",
     "attention_vjp",
 ]

@@ -12,14 +12,17 @@ background section on TF / DF training):
                          the noisy chunk i itself (bidirectional inside it).
 * ``ranges``          -- the mask given directly as query groups with key ranges
                          (paper App. B, sparse custom-mask representation): a list
-                         of (q_end, a0, a1, b0, b1); group g owns query rows
-                         [q_end of g-1, q_end) and admits keys in [a0, a1) and
-                         [b0, b1).  Passed in place of ``offsets``.
+                         of groups (q0, q1, K) where the query interval [q0, q1)
+                         admits every key of every interval [k0, k1) in the list
+                         K = [(k0, k1), ...] (any number R_g >= 0 of ranges).
+                         Passed in place of ``offsets``.
 
 A chunk layout is the prefix array ``offsets`` = [o_0=0 < o_1 < ... < o_N] of
 chunk boundaries within ONE half (TF) or within the whole sequence
-(block-causal).  Nothing here builds ranges or tiles: each (row, column) pair
-is decided from the two tokens' chunk ids and halves, one comparison at a time.
+(block-causal).  Nothing here builds ranges or tiles: for a chunk layout each
+(row, column) pair is decided from the two tokens' chunk ids and halves, and for
+a range list from the row's group and the column's membership in that group's
+key intervals, one comparison at a time.
 """
 import numpy as np
 
@@ -35,14 +38,37 @@ def _chunk_of(tok, offsets):
     return np.searchsorted(offsets, tok, side="right") - 1
 
 
-def expected_length(kind, offsets):
-    """Sequence length implied by a layout (None for the full mask)."""
-    if kind == MASK_FULL:
-        return None
-    if kind == MASK_RANGES:
-        return int(offsets[-1][0])
-    half = int(offsets[-1])
-    return 2 * half if kind == MASK_TEACHER_FORCING else half
+def check_groups(groups, L):
+    """Validate a query-group / key-range list against a sequence of L tokens.
+
+    The App. B representation gives each query group g a contiguous interval
+    Q_g = [q0, q1) and a list K_g of key intervals [k0, k1).  The passage leaves two
+    things implicit, read here as requirements: the query intervals of different
+    groups are disjoint (each task of Algorithm 1 writes the output rows of its
+    group, so a row in two groups would be written twice), and the key intervals of
+    one group are disjoint (Algorithm 1 streams every interval of K_g, so a key in
+    two of them would enter the softmax twice).  Empty intervals (k0 == k1), groups
+    with no key interval and rows in no group are allowed: such rows admit no key.
+    Returns the groups as [(q0, q1, [(k0, k1), ...]), ...].
+    """
+    out = []
+    for g in groups:
+        q0, q1, K = int(g[0]), int(g[1]), [(int(a), int(b)) for a, b in g[2]]
+        if not 0 <= q0 < q1 <= L:
+            raise ValueError(f"query interval [{q0}, {q1}) is not inside [0, {L})")
+        for k0, k1 in K:
+            if not 0 <= k0 <= k1 <= L:
+                raise ValueError(f"key interval [{k0}, {k1}) is not inside [0, {L}]")
+        nonempty = sorted((k0, k1) for k0, k1 in K if k1 > k0)
+        for (a0, a1), (b0, b1) in zip(nonempty, nonempty[1:]):
+            if b0 < a1:
+                raise ValueError(f"key intervals [{a0}, {a1}) and [{b0}, {b1}) of one group overlap")
+        out.append((q0, q1, K))
+    spans = sorted((q0, q1) for q0, q1, _ in out)
+    for (a0, a1), (b0, b1) in zip(spans, spans[1:]):
+        if b0 < a1:
+            raise ValueError(f"query intervals [{a0}, {a1}) and [{b0}, {b1}) overlap")
+    return out
 
 
 def allowed_mask(kind, offsets, L, rows=None, cols=None):
@@ -52,14 +78,13 @@ def allowed_mask(kind, offsets, L, rows=None, cols=None):
     if kind == MASK_FULL:
         return np.ones((rows.size, cols.size), dtype=bool)
     if kind == MASK_RANGES:
-        groups = [tuple(int(v) for v in g) for g in offsets]
-        assert groups[-1][0] == L, "query groups must cover the sequence"
-        q_end = np.array([g[0] for g in groups])
-        g_of_row = np.searchsorted(q_end, rows, side="right")
+        # M[a, b] admits (a, b) iff some group g has a in Q_g and b in one of K_g's intervals
         out = np.zeros((rows.size, cols.size), dtype=bool)
-        for i, g in enumerate(g_of_row):
-            _, a0, a1, b0, b1 = groups[g]
-            out[i] = ((cols >= a0) & (cols < a1)) | ((cols >= b0) & (cols < b1))
+        for q0, q1, K in check_groups(offsets, L):
+            in_q = (rows >= q0) & (rows < q1)
+            for k0, k1 in K:
+                in_k = (cols >= k0) & (cols < k1)
+                out |= in_q[:, None] & in_k[None, :]
         return out
     if kind == MASK_BLOCK_CAUSAL:
         assert L == int(offsets[-1]), "block-causal layout must cover the sequence"

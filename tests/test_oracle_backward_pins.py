@@ -77,7 +77,9 @@ LAYOUTS = [
     (MASK_TEACHER_FORCING, _tf(3, 4), 24),
     (MASK_BLOCK_CAUSAL, [0, 3, 7, 10], 10),
     (MASK_FULL, None, 13),
-    (MASK_RANGES, [(5, 0, 3, 9, 12), (9, 0, 0, 0, 0), (14, 2, 6, 7, 14)], 14),  # group 1: no keys
+    (MASK_RANGES, [(0, 5, [(0, 3), (9, 12)]), (5, 9, []), (9, 14, [(2, 6), (7, 14)])], 14),  # group 1: no keys
+    # three key intervals in one group, adjacent intervals, a row in no group
+    (MASK_RANGES, [(0, 4, [(0, 2), (5, 6), (9, 11)]), (4, 10, [(3, 5), (5, 8)]), (11, 13, [(12, 13), (0, 1)])], 13),
 ]
 
 
@@ -131,14 +133,14 @@ def test_vjp_invariants_and_subsets():
 
 def test_unseen_keys_and_empty_rows_get_zero_gradient():
     # keys 10..13 are admitted by no group; rows 5..8 admit no key
-    groups = [(5, 0, 4, 6, 10), (9, 0, 0, 0, 0), (14, 0, 10, 0, 0)]
+    groups = [(0, 5, [(0, 4), (6, 10)]), (5, 9, []), (9, 14, [(0, 10)])]
     L, D = 14, 8
     Q, K, V, gO = [_rand((1, 1, L, D), 250 + s) for s in range(4)]
     gQ, gK, gV, Delta = attention_vjp(Q, K, V, gO, MASK_RANGES, groups)
     assert np.all(gK[0, 0, 10:] == 0.0) and np.all(gV[0, 0, 10:] == 0.0)
     assert np.all(gQ[0, 0, 5:9] == 0.0) and np.all(Delta[0, 0, 5:9] == 0.0)
     # single-key row: a row that sees only key j has P = e_j, so gV_j gets its cotangent
-    g2 = [(1, 3, 4, 0, 0), (L, 0, L, 0, 0)]
+    g2 = [(0, 1, [(3, 4)]), (1, L, [(0, L)])]
     Z = np.zeros_like(gO)
     Z[0, 0, 0] = gO[0, 0, 0]
     _, _, gV2, _ = attention_vjp(Q, K, V, Z, MASK_RANGES, g2)

@@ -72,19 +72,58 @@ def test_nonuniform_tf_mask_matches_hand_written():
 def test_ranges_mask_reproduces_hand_written_tf_mask():
     # the TF mask of the golden fixture, given as query groups with key ranges
     m, _ = _read_mask("tf_mask_N3_C2.txt")
-    groups = [(2, 0, 2, 0, 0), (4, 0, 4, 0, 0), (6, 0, 6, 0, 0),
-              (8, 0, 0, 6, 8), (10, 0, 2, 8, 10), (12, 0, 4, 10, 12)]
+    groups = [(0, 2, [(0, 2)]), (2, 4, [(0, 4)]), (4, 6, [(0, 6)]),
+              (6, 8, [(0, 0), (6, 8)]), (8, 10, [(0, 2), (8, 10)]), (10, 12, [(0, 4), (10, 12)])]
     assert np.array_equal(allowed_mask(MASK_RANGES, groups, 12), m)
 
 
 def test_ranges_mask_with_empty_group_and_two_ranges():
-    groups = [(1, 0, 0, 0, 0), (3, 1, 2, 4, 5), (5, 0, 5, 0, 0)]
+    groups = [(0, 1, []), (1, 3, [(1, 2), (4, 5)]), (3, 5, [(0, 5)])]
     want = np.array([[0, 0, 0, 0, 0], [0, 1, 0, 0, 1], [0, 1, 0, 0, 1], [1, 1, 1, 1, 1], [1, 1, 1, 1, 1]], bool)
     assert np.array_equal(allowed_mask(MASK_RANGES, groups, 5), want)
 
 
+def _read_groups(name):
+    """The query groups of a golden range-list fixture ('# group: q0 q1 : k0 k1 ...' lines)."""
+    groups = []
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            if line.startswith("# group:"):
+                q, k = line.split(":", 1)[1].split(":")
+                q0, q1 = (int(v) for v in q.split())
+                ks = [int(v) for v in k.split()]
+                groups.append((q0, q1, list(zip(ks[0::2], ks[1::2]))))
+    return groups
+
+
+GENERAL_GROUPS = _read_groups("ranges_general.txt")
+
+
+def test_general_range_list_mask_matches_hand_written():
+    """Groups with four key intervals, none, adjacent ones, an empty one, rows in no group."""
+    m, _ = _read_mask("ranges_general.txt")
+    assert len(GENERAL_GROUPS) == 4 and len(GENERAL_GROUPS[0][2]) == 4 and GENERAL_GROUPS[1][2] == []
+    assert np.array_equal(allowed_mask(MASK_RANGES, GENERAL_GROUPS, 12), m)
+    # the same mask with the adjacent intervals merged, the empty one dropped, groups reordered
+    merged = [GENERAL_GROUPS[3][:2] + ([(0, 3), (11, 12)],), (4, 7, [(2, 6), (9, 10)]), GENERAL_GROUPS[0]]
+    assert np.array_equal(allowed_mask(MASK_RANGES, merged, 12), m)
+    assert count_allowed_pairs(MASK_RANGES, GENERAL_GROUPS, 12) == int(m.sum()) == 2 * 6 + 3 * 5 + 3 * 4
+
+
+@pytest.mark.parametrize("groups,msg", [
+    ([(0, 4, [(0, 3), (2, 5)])], "overlap"),             # key intervals of one group overlap
+    ([(0, 4, [(0, 3)]), (3, 6, [(0, 1)])], "overlap"),    # query intervals overlap
+    ([(0, 4, [(0, 9)])], "inside"),                       # key interval past the end
+    ([(2, 2, [(0, 1)])], "inside"),                       # empty query interval
+    ([(0, 9, [(0, 1)])], "inside"),                       # query interval past the end
+])
+def test_range_lists_outside_the_representation_are_rejected(groups, msg):
+    with pytest.raises(ValueError, match=msg):
+        allowed_mask(MASK_RANGES, groups, 8)
+
+
 def test_fully_masked_rows_give_zero_and_minus_inf():
-    groups = [(2, 0, 0, 0, 0), (5, 0, 5, 0, 0)]
+    groups = [(0, 2, []), (2, 5, [(0, 5)])]
     x = [_rand((1, 1, 5, 4), 200 + s) for s in range(6)]
     O, dO, LSE = attention_jvp(*x, MASK_RANGES, groups)
     assert np.all(O[0, 0, :2] == 0) and np.all(dO[0, 0, :2] == 0) and np.all(LSE[0, 0, :2] == -np.inf)
@@ -204,7 +243,8 @@ def test_tf_two_pass_identity(N, C):
 
 @pytest.mark.parametrize("kind,offsets,L", [(MASK_TEACHER_FORCING, _tf(3, 4), 24),
                                             (MASK_BLOCK_CAUSAL, [0, 3, 7, 10], 10),
-                                            (MASK_FULL, None, 13)])
+                                            (MASK_FULL, None, 13),
+                                            (MASK_RANGES, GENERAL_GROUPS, 12)])
 def test_tangent_vs_central_finite_differences(kind, offsets, L):
     B, H, D = 1, 2, 8
     x = [_rand((B, H, L, D), 40 + s) for s in range(6)]
@@ -222,7 +262,8 @@ def test_tangent_vs_central_finite_differences(kind, offsets, L):
 @pytest.mark.parametrize("kind,offsets,L,D", [(MASK_TEACHER_FORCING, _tf(2, 3), 12, 4),
                                               (MASK_TEACHER_FORCING, [0, 1, 4, 6], 12, 3),
                                               (MASK_BLOCK_CAUSAL, [0, 2, 5], 5, 4),
-                                              (MASK_FULL, None, 7, 5)])
+                                              (MASK_FULL, None, 7, 5),
+                                              (MASK_RANGES, GENERAL_GROUPS, 12, 3)])
 def test_closed_form_vs_dual_numbers(kind, offsets, L, D):
     B, H = 1, 2
     x = [_rand((B, H, L, D), 50 + s) for s in range(6)]
