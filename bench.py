@@ -62,14 +62,14 @@ def kernel_source_hash():
 
 def zero_clean_flop(groups, half, D):
     """Flop per (batch, head) of the zero-clean JVP from the query-group table
-    [(q0, q1, a0, a1, b0, b1)]: 4D per pair of a clean query, 8D per (noisy query,
+    [(q0, q1, [(k0, k1), ...])]: 4D per pair of a clean query, 8D per (noisy query,
     clean key) pair, 12D per (noisy query, noisy key) pair."""
     total = 0
-    for q0, q1, a0, a1, b0, b1 in groups:
+    for q0, q1, ks in groups:
         for r0, r1 in ((q0, min(q1, half)), (max(q0, half), q1)):
             if r1 <= r0:
                 continue
-            for k0, k1 in ((a0, a1), (b0, b1)):
+            for k0, k1 in ks:
                 clean_keys = max(0, min(k1, half) - k0)
                 noisy_keys = max(0, k1 - max(k0, half))
                 if r1 <= half:

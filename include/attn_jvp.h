@@ -19,8 +19,8 @@
  * ---------------------------------------
  * - Tensors are contiguous row-major [B, H, L, D] (batch, head, token, head_dim),
  *   all with the same dtype (ATTN_DTYPE_*); LSE is fp32 [B, H, L].
- * - Tensor pointers are DEVICE pointers; the chunk layout is a HOST struct whose
- *   offsets array is HOST memory, read during the call only.
+ * - Tensor pointers are DEVICE pointers; the mask layout is a HOST struct whose
+ *   arrays are HOST memory, read during the call only.
  * - softmax_scale <= 0 selects s = 1/sqrt(D).
  * - Work is enqueued on `stream` (a hipStream_t passed as void*, NULL = default
  *   stream) and the call returns without synchronising: outputs are valid once
@@ -76,25 +76,40 @@ enum {
 #define ATTN_MAX_CHUNKS 64
 /* largest number of query groups of an ATTN_MASK_RANGES layout */
 #define ATTN_MAX_GROUPS 128
+/* largest number of key ranges, over all groups, after a layout's ranges are
+ * normalised (empty ranges dropped, touching ranges of a group merged) */
+#define ATTN_MAX_RANGES 256
 
-/* Chunk layout of the mask.  chunk_offsets (HOST memory) holds num_chunks + 1
+/* Mask layout.
+ *
+ * Block-causal and teacher-forcing: chunk_offsets (HOST memory) holds num_chunks + 1
  * strictly increasing prefix offsets 0 = o_0 < o_1 < ... < o_N of the chunk
  * boundaries within ONE half of the TF sequence (teacher forcing) or within the
  * sequence (block-causal).  Uniform chunks of C tokens use o_i = i * C.
  *
  * ATTN_MASK_RANGES gives the query-group / key-range representation directly (paper
- * App. B, "Sparse custom-mask representation"): num_chunks = G query groups
- * (1..ATTN_MAX_GROUPS) and `ranges` (HOST memory) holds 5 G ints, per group
- * q_end, a0, a1, b0, b1: group g owns query rows [q_end(g-1), q_end(g)) (q_end(-1) = 0,
- * strictly increasing, q_end(G-1) = L) and admits keys in [a0, a1) and [b0, b1)
- * (0 <= begin <= end <= L; an empty range has begin == end; the two ranges must not
- * overlap).  A group with two empty ranges has fully masked rows: O = 0, dO = 0,
- * LSE = -inf. */
+ * App. B, "Sparse custom-mask representation": query group g owns the query interval
+ * Q_g = [q_g, q_{g+1}) and admits the keys of its list K_g of R_g >= 0 key intervals).
+ * All arrays are HOST memory, read during the call only:
+ *   num_chunks     = G query groups (1 .. ATTN_MAX_GROUPS)
+ *   chunk_offsets  = G + 1 query-group bounds 0 = q_0 < q_1 < ... < q_G = L (the groups
+ *                    tile the sequence; a row that should see no key belongs to a group
+ *                    with no key range)
+ *   range_offsets  = G + 1 non-decreasing ints, range_offsets[0] = 0: the key ranges of
+ *                    group g are entries range_offsets[g] .. range_offsets[g + 1] - 1
+ *   ranges         = 2 * range_offsets[G] ints, k0 k1 per key range [k0, k1), with
+ *                    0 <= k0 <= k1 <= L; the ranges of one group may come in any order,
+ *                    may be empty (k0 == k1) or touch, but must not overlap (a key in two
+ *                    ranges of a group would enter the softmax twice)
+ * Rows of a group with no (non-empty) key range are fully masked: O = 0, dO = 0,
+ * LSE = -inf.  After empty ranges are dropped and touching ones merged, at most
+ * ATTN_MAX_RANGES ranges may remain; beyond that the layout is ATTN_ERR_INVALID. */
 typedef struct attn_chunk_layout {
   int32_t kind;                  /* ATTN_MASK_* */
   int32_t num_chunks;            /* N (chunks) or G (groups, ATTN_MASK_RANGES); ignored for FULL */
-  const int32_t* chunk_offsets;  /* N + 1 host ints (block-causal / TF only; else may be NULL) */
-  const int32_t* ranges;         /* 5 G host ints (ATTN_MASK_RANGES only; else may be NULL) */
+  const int32_t* chunk_offsets;  /* N + 1 chunk offsets, or G + 1 query-group bounds (RANGES) */
+  const int32_t* range_offsets;  /* G + 1 range offsets (ATTN_MASK_RANGES only; else may be NULL) */
+  const int32_t* ranges;         /* 2 * range_offsets[G] ints (ATTN_MASK_RANGES only; else may be NULL) */
 } attn_chunk_layout;
 
 /* Fused masked attention forward + JVP (paper App. B, Algorithm 1).
@@ -151,41 +166,43 @@ int attn_fwd(int dtype, int B, int H, int L, int D,
  *   out: gQ, gK, gV            device [B, H, L, D], dtype `dtype`
  *        Delta                 device fp32 [B, H, L]: rowsum(gO o O) (written by the
  *                              first of the two kernels, read by the second)
- * Same conventions and error behaviour as attn_jvp_fwd.  The key-side pass needs the
- * mask transposed into key groups with at most two query ranges each and at most
- * ATTN_MAX_GROUPS of them: always so for the full, block-causal and teacher-forcing
- * layouts; an ATTN_MASK_RANGES layout for which it is not so is ATTN_ERR_UNSUPPORTED.
- * Deterministic (no atomics): two launches on `stream`. */
+ * Same conventions and error behaviour as attn_jvp_fwd; every layout the forward
+ * accepts is accepted.  Deterministic (no atomics): two launches on `stream`. */
 int attn_bwd(int dtype, int B, int H, int L, int D,
              const void* Q, const void* K, const void* V, const void* O, const void* gO,
              const float* LSE, const attn_chunk_layout* layout, float softmax_scale,
              void* gQ, void* gK, void* gV, float* Delta, void* stream);
 
-/* Host only.  The mask transposed into key groups, in the layout of
- * attn_query_groups with keys and queries swapped: 6 int32 per group, k0, k1, a0, a1,
- * b0, b1 (keys [k0, k1) are admitted by the queries in [a0, a1) and [b0, b1)).
- * Returns the number of groups, or -1 (ATTN_ERR_UNSUPPORTED message if the transpose
- * does not fit the two-range form, ATTN_ERR_INVALID for a bad layout or buffer). */
-int attn_key_groups(const attn_chunk_layout* layout, int L, int32_t* out, int max_groups);
+/* Host only.  Query-block plan of key tile `ktile` of the backward's key-tile pass
+ * (keys [ktile*K, ktile*K + K) with K = 128, query blocks of 64 rows) as the bf16
+ * kernel executes it: the visited query-block indices in visiting order go to
+ * blocks[], and full[i] = 1 if every query of block i admits every key of the tile
+ * (no per-element mask applied), else 0.  Returns the number of visited blocks, or
+ * -1 on an invalid layout, tile index or a too-small buffer (capacity `cap`). */
+int attn_key_tile_plan(const attn_chunk_layout* layout, int L, int ktile, int32_t* blocks, int32_t* full, int cap);
 
 /* Host only.  Number of admissible (query, key) pairs of the layout over a
- * sequence of L tokens, i.e. the pairs whose work is counted in throughput
- * figures.  Returns -1 (and sets the error message) for an invalid layout. */
+ * sequence of L tokens: the pairs whose work the throughput figures count (the
+ * entries of the mask M of the masked-attention equation, paper App. B, that are 0
+ * rather than -inf).  Returns -1 (and sets the error message) for an invalid layout. */
 int64_t attn_count_unmasked_pairs(const attn_chunk_layout* layout, int L);
 
 /* Host only.  Number of (query, key) pairs the bf16 kernel actually evaluates
- * for this layout (whole key blocks, including masked lanes of partial blocks),
- * for one (batch, head).  Returns -1 on an invalid layout or head_dim. */
+ * for this layout, for one (batch, head): whole key blocks of the tile plans,
+ * including the masked lanes of partial blocks (the key/value tiles streamed by
+ * Algorithm 1's inner loop, paper App. B, under this library's tiling).  Returns -1
+ * on an invalid layout or head_dim. */
 int64_t attn_count_computed_pairs(const attn_chunk_layout* layout, int L, int D);
 
 /* Host only.  The query-group / key-range table derived from the layout (paper
- * App. B, "Sparse custom-mask representation": query interval [q0, q1) with a
- * list of admissible key intervals; here at most two per group).  Writes
- * 6 int32 per group: q0, q1, a0, a1, b0, b1 (key ranges [a0,a1) and [b0,b1),
- * an empty range has begin == end) into `out` (capacity max_groups groups).
- * Returns the number of groups, or -1 on an invalid layout or a too-small
- * buffer. */
-int attn_query_groups(const attn_chunk_layout* layout, int L, int32_t* out, int max_groups);
+ * App. B, "Sparse custom-mask representation": query interval [q_g, q_{g+1}) with a
+ * list of admissible key intervals), normalised: the ranges of each group sorted,
+ * without empty ones, touching ones merged.  Writes G + 1 bounds, G + 1 range offsets
+ * and 2 R ints k0 k1 (R = range_offsets[G]) in the form of an ATTN_MASK_RANGES layout;
+ * capacities max_groups groups and max_ranges ranges.  Returns G, or -1 on an
+ * invalid layout or a too-small buffer. */
+int attn_query_groups(const attn_chunk_layout* layout, int L, int32_t* bounds, int32_t* range_offsets,
+                      int32_t* ranges, int max_groups, int max_ranges);
 
 /* Host only.  Shape of the work decomposition of the bf16 JVP kernels: query rows
  * per work-group tile and keys per streamed key block (the forward-only kernel takes

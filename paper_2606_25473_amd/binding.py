@@ -25,9 +25,14 @@ class AttnError(RuntimeError):
         self.code = code
 
 
+MAX_GROUPS = 128
+MAX_RANGES = 256
+
+
 class _Layout(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("num_chunks", ctypes.c_int32),
                 ("chunk_offsets", ctypes.POINTER(ctypes.c_int32)),
+                ("range_offsets", ctypes.POINTER(ctypes.c_int32)),
                 ("ranges", ctypes.POINTER(ctypes.c_int32))]
 
 
@@ -60,13 +65,14 @@ def load_library():
     lib.attn_bwd.argtypes = [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp,
                              ctypes.POINTER(_Layout), ctypes.c_float, _vp, _vp, _vp, _vp, _vp]
     lib.attn_bwd.restype = _i
-    lib.attn_key_groups.argtypes = [ctypes.POINTER(_Layout), _i, ctypes.POINTER(ctypes.c_int32), _i]
-    lib.attn_key_groups.restype = _i
+    _ip = ctypes.POINTER(ctypes.c_int32)
+    lib.attn_key_tile_plan.argtypes = [ctypes.POINTER(_Layout), _i, _i, _ip, _ip, _i]
+    lib.attn_key_tile_plan.restype = _i
     lib.attn_count_unmasked_pairs.argtypes = [ctypes.POINTER(_Layout), _i]
     lib.attn_count_unmasked_pairs.restype = ctypes.c_int64
     lib.attn_count_computed_pairs.argtypes = [ctypes.POINTER(_Layout), _i, _i]
     lib.attn_count_computed_pairs.restype = ctypes.c_int64
-    lib.attn_query_groups.argtypes = [ctypes.POINTER(_Layout), _i, ctypes.POINTER(ctypes.c_int32), _i]
+    lib.attn_query_groups.argtypes = [ctypes.POINTER(_Layout), _i, _ip, _ip, _ip, _i, _i]
     lib.attn_query_groups.restype = _i
     lib.attn_tile_shape.argtypes = [ctypes.POINTER(_i), ctypes.POINTER(_i)]
     lib.attn_tile_shape.restype = None
@@ -81,22 +87,36 @@ def load_library():
     return lib
 
 
+def _i32(vals):
+    return (ctypes.c_int32 * max(1, len(vals)))(*vals)
+
+
 def make_layout(kind, offsets=None):
     """C layout struct for mask ``kind`` ('full' | 'block_causal' | 'teacher_forcing' |
     'ranges', or its code).  ``offsets``: chunk prefix offsets, or for 'ranges' the
-    query groups [(q_end, a0, a1, b0, b1), ...]."""
+    query groups [(q0, q1, [(k0, k1), ...]), ...] in increasing order, each starting
+    where the previous one ends (rows that see no key form a group with no range)."""
     code = MASK_KINDS[kind] if isinstance(kind, str) else int(kind)
     if code == MASK_KINDS["ranges"]:
-        groups = [tuple(int(v) for v in g) for g in (offsets or [])]
-        flat = [v for g in groups for v in g]
-        arr = (ctypes.c_int32 * max(1, len(flat)))(*flat)
-        lay = _Layout(code, len(groups), None, arr)
-        lay._keep = arr
+        groups = list(offsets or [])
+        bounds, roffs, flat = [], [0], []
+        for i, (q0, q1, ks) in enumerate(groups):
+            if i == 0:
+                bounds.append(int(q0))
+            elif int(q0) != bounds[-1]:
+                raise ValueError(f"query group {i} starts at {q0}, not where group {i - 1} ends ({bounds[-1]})")
+            bounds.append(int(q1))
+            for k0, k1 in ks:
+                flat += [int(k0), int(k1)]
+            roffs.append(len(flat) // 2)
+        arrs = (_i32(bounds), _i32(roffs), _i32(flat))
+        lay = _Layout(code, len(groups), arrs[0], arrs[1], arrs[2])
+        lay._keep = arrs  # keep the arrays alive with the struct
         return lay
     offs = [] if offsets is None else [int(x) for x in offsets]
-    arr = (ctypes.c_int32 * max(1, len(offs)))(*offs) if offs else None
-    lay = _Layout(code, max(0, len(offs) - 1), arr if arr is not None else None, None)
-    lay._keep = arr  # keep the offsets array alive with the struct
+    arr = _i32(offs) if offs else None
+    lay = _Layout(code, max(0, len(offs) - 1), arr, None, None)
+    lay._keep = arr
     return lay
 
 
@@ -132,6 +152,20 @@ def _check_inputs(ts, shape=None):
             raise ValueError("inputs must be contiguous")
 
 
+def _check_out(t, name, shape, dtype, device):
+    """A caller-supplied output: contiguous, of the shape, dtype and device the call writes."""
+    if not isinstance(t, torch.Tensor) or t.device != device or t.dtype != dtype \
+            or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"out tensor {name} must be a contiguous {dtype} tensor of shape {tuple(shape)} on {device}")
+
+
+def _check_outs(outs, specs, q):
+    if len(outs) != len(specs):
+        raise ValueError(f"out must hold {len(specs)} tensors")
+    for t, (name, shape, dtype) in zip(outs, specs):
+        _check_out(t, name, shape, dtype, q.device)
+
+
 def attn_jvp_fwd(q, k, v, dq, dk, dv, kind="teacher_forcing", offsets=None, scale=None,
                  out=None, stream=None):
     """(O, dO, LSE) of masked softmax attention and its forward-mode tangent.
@@ -147,6 +181,7 @@ def attn_jvp_fwd(q, k, v, dq, dk, dv, kind="teacher_forcing", offsets=None, scal
         o, do = torch.empty_like(q), torch.empty_like(q)
         lse = torch.empty((B, H, L), device=q.device, dtype=torch.float32)
     else:
+        _check_outs(out, [("O", q.shape, q.dtype), ("dO", q.shape, q.dtype), ("LSE", (B, H, L), torch.float32)], q)
         o, do, lse = out
     lay = make_layout(kind, offsets)
     st = stream if stream is not None else torch.cuda.current_stream(q.device)
@@ -179,6 +214,7 @@ def attn_jvp_fwd_zero_clean(q, k, v, dqn, dkn, dvn, offsets, scale=None, out=Non
         don = torch.empty(nshape, device=q.device, dtype=q.dtype)
         lse = torch.empty((B, H, L), device=q.device, dtype=torch.float32)
     else:
+        _check_outs(out, [("O", q.shape, q.dtype), ("dOn", nshape, q.dtype), ("LSE", (B, H, L), torch.float32)], q)
         o, don, lse = out
     lay = make_layout("teacher_forcing", offsets)
     st = stream if stream is not None else torch.cuda.current_stream(q.device)
@@ -200,6 +236,7 @@ def attn_fwd(q, k, v, kind="teacher_forcing", offsets=None, scale=None, out=None
         o = torch.empty_like(q)
         lse = torch.empty((B, H, L), device=q.device, dtype=torch.float32)
     else:
+        _check_outs(out, [("O", q.shape, q.dtype), ("LSE", (B, H, L), torch.float32)], q)
         o, lse = out
     lay = make_layout(kind, offsets)
     st = stream if stream is not None else torch.cuda.current_stream(q.device)
@@ -227,6 +264,8 @@ def attn_bwd(q, k, v, o, go, lse, kind="teacher_forcing", offsets=None, scale=No
         gq, gk, gv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
         delta = torch.empty((B, H, L), device=q.device, dtype=torch.float32)
     else:
+        _check_outs(out, [("gQ", q.shape, q.dtype), ("gK", q.shape, q.dtype), ("gV", q.shape, q.dtype),
+                          ("Delta", (B, H, L), torch.float32)], q)
         gq, gk, gv, delta = out
     lay = make_layout(kind, offsets)
     st = stream if stream is not None else torch.cuda.current_stream(q.device)
@@ -238,14 +277,15 @@ def attn_bwd(q, k, v, o, go, lse, kind="teacher_forcing", offsets=None, scale=No
     return gq, gk, gv, delta
 
 
-def key_groups(kind, offsets, L):
-    """The mask transposed into key groups [(k0, k1, a0, a1, b0, b1), ...] (host-only call)."""
-    cap = 2 * MAX_CHUNKS
-    buf = (ctypes.c_int32 * (6 * cap))()
-    n = load_library().attn_key_groups(ctypes.byref(make_layout(kind, offsets)), int(L), buf, cap)
+def _read_table(fn, kind, offsets, L):
+    bounds = (ctypes.c_int32 * (MAX_GROUPS + 1))()
+    roffs = (ctypes.c_int32 * (MAX_GROUPS + 1))()
+    ranges = (ctypes.c_int32 * (2 * MAX_RANGES))()
+    n = fn(ctypes.byref(make_layout(kind, offsets)), int(L), bounds, roffs, ranges, MAX_GROUPS, MAX_RANGES)
     if n < 0:
         raise AttnError(1, last_error())
-    return [tuple(buf[6 * g:6 * g + 6]) for g in range(n)]
+    return [(bounds[g], bounds[g + 1], [(ranges[2 * r], ranges[2 * r + 1]) for r in range(roffs[g], roffs[g + 1])])
+            for g in range(n)]
 
 
 def count_unmasked_pairs(kind, offsets, L):
@@ -265,13 +305,9 @@ def count_computed_pairs(kind, offsets, L, D=128):
 
 
 def query_groups(kind, offsets, L):
-    """Query-group table [(q0, q1, a0, a1, b0, b1), ...] derived by the library."""
-    cap = 2 * MAX_CHUNKS
-    buf = (ctypes.c_int32 * (6 * cap))()
-    n = load_library().attn_query_groups(ctypes.byref(make_layout(kind, offsets)), int(L), buf, cap)
-    if n < 0:
-        raise AttnError(1, last_error())
-    return [tuple(buf[6 * g:6 * g + 6]) for g in range(n)]
+    """Query-group table [(q0, q1, [(k0, k1), ...]), ...] derived by the library (normalised:
+    each group's ranges sorted, empty ones dropped, touching ones merged)."""
+    return _read_table(load_library().attn_query_groups, kind, offsets, L)
 
 
 def tile_shape():
@@ -291,6 +327,19 @@ def tile_order(kind, offsets, L, zero_clean=False):
     if n < 0:
         raise AttnError(1, last_error())
     return list(buf[:n])
+
+
+def key_tile_plan(kind, offsets, L, ktile):
+    """[(query_block, is_full), ...] visited by key tile ``ktile`` of the bf16 backward
+    (128 keys per tile, 64-row query blocks)."""
+    cap = (int(L) + 63) // 64 + 8
+    blocks = (ctypes.c_int32 * cap)()
+    full = (ctypes.c_int32 * cap)()
+    n = load_library().attn_key_tile_plan(ctypes.byref(make_layout(kind, offsets)), int(L), int(ktile),
+                                          blocks, full, cap)
+    if n < 0:
+        raise AttnError(1, last_error())
+    return [(blocks[i], bool(full[i])) for i in range(n)]
 
 
 def tile_plan(kind, offsets, L, qtile):

@@ -11,8 +11,8 @@
 //    plan) and accumulates gQ^T = K^T gS^T;
 //  - key-tile pass: a work-group owns 128 keys (4 waves x 32) and two halves of each
 //    64-row query block (waves 0..3 the first 32 rows, 4..7 the second), streams the
-//    query blocks that see its keys (the plan of the transposed, key-group table)
-//    through a three-stage LDS ring (block it+2 loads while block it is used), and
+//    query blocks that see its keys (the query groups admitting any of them) through a
+//    three-stage LDS ring (block it+2 loads while block it is used), and
 //    accumulates gV^T = gO^T P and gK^T = Q^T gS; the two halves are summed at the end.
 //    Each wave keeps the K operands of its 32 keys in registers (read once from LDS), so
 //    the LDS holds only the V tile and the three stages.
@@ -87,12 +87,10 @@ void attn_bwd_dq_kernel(const BwdArgs a) {
 
   const int qrow = wave * 32 + (lane & 31);
   const int row = q0 + qrow;
-  int ra0 = 0, ra1 = 0, rb0 = 0, rb1 = 0;
-  for (int g = plan.g_first; g <= plan.g_last; ++g) {
-    if (row >= group_q_begin(a.gt, g) && row < a.gt.q_end[g]) {
-      ra0 = a.gt.a0[g]; ra1 = a.gt.a1[g]; rb0 = a.gt.b0[g]; rb1 = a.gt.b1[g];
-    }
-  }
+  // groups holding the wave's 32 rows (uniform; partial blocks form the row's mask bits
+  // from their key ranges)
+  const int wrow0 = imin(q0 + wave * 32, L - 1);
+  const int wg0 = find_group(a.gt, wrow0), wg1 = find_group(a.gt, imin(wrow0 + 31, L - 1));
 
   // Q^T and gO^T as B operands in registers (lane: row l%32, d = 16 s + 8 (l/32) + 0..7);
   // rows past the end are clamped to the last row (their results are not stored)
@@ -201,13 +199,10 @@ void attn_bwd_dq_kernel(const BwdArgs a) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) p[i] = __builtin_amdgcn_exp2f(fmaf(S[i], c2, -lse2));
     if (!block_is_full(plan, k0, QBC, L)) {  // one uniform branch around the whole mask
+      // the lane holds keys k0 + 8 (i/4) + 4 hh + i%4
+      const uint32_t bits = row_bits(a.gt, wg0, wg1, row, k0) >> (4 * hh);
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int key = k0 + 8 * (i >> 2) + 4 * hh + (i & 3);
-        const bool ok = (unsigned)(key - ra0) < (unsigned)(ra1 - ra0) ||
-                        (unsigned)(key - rb0) < (unsigned)(rb1 - rb0);
-        p[i] = ok ? p[i] : 0.f;
-      }
+      for (int i = 0; i < 16; ++i) p[i] = ((bits >> (8 * (i >> 2) + (i & 3))) & 1u) ? p[i] : 0.f;
     }
 #pragma unroll
     for (int i = 0; i < 16; ++i) gs[i] = p[i] * (GP[i] - delta);
@@ -332,20 +327,15 @@ void attn_bwd_dkdv_kernel(const BwdArgs a) {
   const float* __restrict__ LSEg = a.LSE + (size_t)bh * L;
   const float* __restrict__ Dg = a.Delta + (size_t)bh * L;
 
-  // plan over the key-group table: the query blocks that see the tile's keys
+  // plan over the query-group table: the query blocks of the groups that admit some key
+  // of the tile
   const int k0 = ktile * KT;
   const int k1 = k0 + KT < L ? k0 + KT : L;
-  const TilePlan plan = plan_tile(a.gt, k0, k1, QB);
+  const TilePlan plan = plan_key_tile(a.gt, k0, k1, QB);
   const int nblk = plan_num_blocks(plan);
 
   const int krow = kw * 32 + (lane & 31);  // this lane's key within the tile
   const int key = k0 + krow;
-  int ra0 = 0, ra1 = 0, rb0 = 0, rb1 = 0;  // query ranges that admit this key
-  for (int g = plan.g_first; g <= plan.g_last; ++g) {
-    if (key >= group_q_begin(a.gt, g) && key < a.gt.q_end[g]) {
-      ra0 = a.gt.a0[g]; ra1 = a.gt.a1[g]; rb0 = a.gt.b0[g]; rb1 = a.gt.b1[g];
-    }
-  }
 
   constexpr int RPI = 1024 / G::ROWB;
   const int dma_r = (lane * 16) / G::ROWB;
@@ -464,13 +454,10 @@ void attn_bwd_dkdv_kernel(const BwdArgs a) {
       }
     }
     if (!block_is_full(plan, q0b, QB, L)) {  // one uniform branch around the whole mask
+      // the lane holds queries q0b + 32 qh + 8 (i/4) + 4 hh + i%4
+      const uint32_t bits = key_bits(a.gt, key, q0b + 32 * qh, L) >> (4 * hh);
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int q = q0b + 32 * qh + 8 * (i >> 2) + 4 * hh + (i & 3);
-        const bool ok = (unsigned)(q - ra0) < (unsigned)(ra1 - ra0) ||
-                        (unsigned)(q - rb0) < (unsigned)(rb1 - rb0);
-        p[i] = ok ? p[i] : 0.f;
-      }
+      for (int i = 0; i < 16; ++i) p[i] = ((bits >> (8 * (i >> 2) + (i & 3))) & 1u) ? p[i] : 0.f;
     }
     float gs[16];
 #pragma unroll
@@ -576,7 +563,7 @@ __global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_bwd_simt_dq_kerne
   const float* O = (const float*)a.O + head;
   const float* gO = (const float*)a.gO + head;
   const int g = find_group(a.gt, row);
-  const int rng[2][2] = {{a.gt.a0[g], a.gt.a1[g]}, {a.gt.b0[g], a.gt.b1[g]}};
+  const int r_first = a.gt.r_begin[g], r_last = a.gt.r_begin[g + 1];  // the group's key ranges
   float q[E], go[E], acc[E];
   float dp = 0.f;
 #pragma unroll
@@ -590,8 +577,8 @@ __global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_bwd_simt_dq_kerne
   const float delta = wave_sum(dp);
   const float lse = a.LSE[(size_t)bh * L + row];
   const float sc = a.scale;
-  for (int ri = 0; ri < 2; ++ri) {
-    for (int k = rng[ri][0]; k < rng[ri][1]; ++k) {
+  for (int ri = r_first; ri < r_last; ++ri) {
+    for (int k = a.gt.k[2 * ri]; k < a.gt.k[2 * ri + 1]; ++k) {
       float s = 0.f, gp = 0.f;
 #pragma unroll
       for (int e = 0; e < E; ++e) {
@@ -611,7 +598,7 @@ __global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_bwd_simt_dq_kerne
   if (lane == 0) a.Delta[(size_t)bh * L + row] = delta;
 }
 
-// One wave per key: gK and gV over the query ranges that admit the key.
+// One wave per key: gK and gV over the queries of the groups that admit the key.
 template <int D>
 __global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_bwd_simt_dkdv_kernel(const BwdArgs a) {
   constexpr int E = D / 64;
@@ -627,8 +614,6 @@ __global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_bwd_simt_dkdv_ker
   const float* gO = (const float*)a.gO + head;
   const float* LSE = a.LSE + (size_t)bh * L;
   const float* Dl = a.Delta + (size_t)bh * L;
-  const int g = find_group(a.gt, key);  // key-group table
-  const int rng[2][2] = {{a.gt.a0[g], a.gt.a1[g]}, {a.gt.b0[g], a.gt.b1[g]}};
   float k[E], v[E], gk[E], gv[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) {
@@ -638,8 +623,12 @@ __global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_bwd_simt_dkdv_ker
     gv[e] = 0.f;
   }
   const float sc = a.scale;
-  for (int ri = 0; ri < 2; ++ri) {
-    for (int q = rng[ri][0]; q < rng[ri][1]; ++q) {
+  // the queries of every group that admits this key
+  for (int g = 0; g < a.gt.n; ++g) {
+    bool hit = false;
+    for (int ri = a.gt.r_begin[g]; ri < a.gt.r_begin[g + 1]; ++ri) hit |= key >= a.gt.k[2 * ri] && key < a.gt.k[2 * ri + 1];
+    if (!hit) continue;
+    for (int q = group_q_begin(a.gt, g); q < a.gt.q_end[g]; ++q) {
       float s = 0.f, gp = 0.f;
 #pragma unroll
       for (int e = 0; e < E; ++e) {

@@ -130,21 +130,14 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   // (kZeroClean) the plan visits key blocks in increasing key order: the first ntk of
   // them hold no key >= t0
   int ntk = 0;
-  if constexpr (ZC) {
-    const int kc = t0 / BC;
-    ntk = imin(imax(kc - plan.blk_begin0, 0), plan.blk_end0 - plan.blk_begin0) +
-          imin(imax(kc - plan.blk_begin1, 0), plan.blk_end1 - plan.blk_begin1);
-  }
+  if constexpr (ZC) ntk = plan_blocks_below(plan, t0 / BC);
 
-  // ---- this lane's query row and its admissible key ranges
+  // ---- this lane's query row, and the groups holding the wave's 32 rows (uniform: the
+  // per-row mask of partial blocks is formed from their key ranges on the scalar unit)
   const int qrow = wave * 32 + (lane & 31);   // row within the tile
   const int row = q0 + qrow;
-  int ra0 = 0, ra1 = 0, rb0 = 0, rb1 = 0;
-  for (int g = plan.g_first; g <= plan.g_last; ++g) {
-    if (row >= group_q_begin(a.gt, g) && row < a.gt.q_end[g]) {
-      ra0 = a.gt.a0[g]; ra1 = a.gt.a1[g]; rb0 = a.gt.b0[g]; rb1 = a.gt.b1[g];
-    }
-  }
+  const int wrow0 = imin(q0 + wave * 32, L - 1);
+  const int wg0 = find_group(a.gt, wrow0), wg1 = find_group(a.gt, imin(wrow0 + 31, L - 1));
 
   // ---- Q^T as B operand in registers: lane l holds row l%32, d = 16 s + 8 (l/32) + 0..7
   bf16x8 qop[G::KS];
@@ -289,13 +282,12 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
   // (k+1) mod 3 (whose block, k-2, was last read in interval k-1) during interval k
   // only.  The score phase runs at raised wave priority, so that its MFMAs go first and
   // its softmax overlaps the other wave's output MFMAs.
-  constexpr bool PP = NW == 8;  // (two waves of a work-group per SIMD)
-  constexpr int DIST = PP ? 1 : 2;  // prefetch distance in blocks
+  constexpr bool PP = NW == 8;  // (two waves of a work-group per SIMD; prefetch distance 1, else 2)
   static_assert(!ZC || PP, "zero-clean load counts vary by block: only full waits are correct");
   const bool late = PP && wave >= NW / 2;
-  // barrier of block k: every own load but those of block k+DIST has landed (lockstep:
-  // N per wave; D = 128: one per tile and wave; D = 64: waves 0..3 issue one, the others
-  // none), every LDS read has returned
+  // barrier of block k: every own load but those of the block one prefetch distance
+  // ahead has landed (lockstep: N per wave; D = 128: one per tile and wave; D = 64:
+  // waves 0..3 issue one, the others none), every LDS read has returned
   auto end_iteration = [&]() {
     constexpr int N = PP ? 0 : (JVP ? 4 : 2) * ((G::IPT + NW - 1) / NW);
     static_assert(N == 0 || N == 2 || N == 4, "vmcnt immediate below");
@@ -352,7 +344,8 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
                   unsigned next_stage) -> bool {
     constexpr bool TK = JVP && decltype(tk)::value;
     constexpr int C = decltype(am)::value;  // stage index known at compile time, or -1
-    // prefetch block it+DIST (redone, with the same data, when the block is redone).
+    // prefetch the block one prefetch distance ahead (redone, with the same data, when
+    // the block is redone).
     // Lockstep: a fixed number of loads per iteration, indices past the end clamped (that
     // stage is never read).
     if constexpr (PP) {
@@ -399,11 +392,12 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
       dsv[i] = JVP ? dS[i] : 0.f;
     }
     if (!block_is_full(plan, k0, BC, L)) {
+      // admitted keys of the block for this lane's row; the lane holds keys
+      // k0 + 8 (i/4) + 4 hh + i%4
+      const uint32_t bits = row_bits(a.gt, wg0, wg1, row, k0) >> (4 * hh);
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int key = k0 + 8 * (i >> 2) + 4 * hh + (i & 3);
-        const bool ok = (unsigned)(key - ra0) < (unsigned)(ra1 - ra0) ||
-                        (unsigned)(key - rb0) < (unsigned)(rb1 - rb0);
+        const bool ok = (bits >> (8 * (i >> 2) + (i & 3))) & 1u;
         sv[i] = ok ? sv[i] : -INFINITY;
         dsv[i] = ok ? dsv[i] : 0.f;
       }
@@ -443,7 +437,7 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
     return false;
   };
 
-  // prologue: dQ of the query tile, then the first DIST key blocks
+  // prologue: dQ of the query tile, then the first key blocks (one per unit of prefetch distance)
   const unsigned st_lds = __builtin_amdgcn_readfirstlane(lds_addr(stages));
   if constexpr (JVP) {
     const unsigned dq_lds = __builtin_amdgcn_readfirstlane(lds_addr(sdQ));
@@ -474,7 +468,7 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
     if constexpr (ZC) {
       // key blocks below t0: no dK, dV terms
       while (it < ntk) {
-        const int nxt = PP ? (cur == 2 ? 0 : cur + 1) : (cur == 0 ? 2 : cur - 1);  // (it + DIST) mod 3
+        const int nxt = PP ? (cur == 2 ? 0 : cur + 1) : (cur == 0 ? 2 : cur - 1);  // its prefetch stage
         const char* cs = stages + cur * SB;
         rescale = step(Tag<false>{}, IC<-1>{}, it, cs, cs + TB, cs + 2 * TB, cs + 2 * TB + TBJ,
                        st_lds + (unsigned)(nxt * SB));
@@ -512,7 +506,7 @@ __device__ __forceinline__ void tile_body(const AttnArgs& a, const int bh, const
       }
     } else if (!rescale) {
       while (it < nblk) {
-        const int nxt = PP ? (cur == 2 ? 0 : cur + 1) : (cur == 0 ? 2 : cur - 1);  // (it + DIST) mod 3
+        const int nxt = PP ? (cur == 2 ? 0 : cur + 1) : (cur == 0 ? 2 : cur - 1);  // its prefetch stage
         char* cs = stages + cur * SB;
         if constexpr (ZC) {
           // a block straddling t0: clear the tangent rows of its keys below t0 (once per

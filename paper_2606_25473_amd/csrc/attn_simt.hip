@@ -45,7 +45,7 @@ __global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_simt_kernel(const
   const float* dV = (const float*)a.dV + thead;
 
   const int g = find_group(a.gt, row);
-  const int rng[2][2] = {{a.gt.a0[g], a.gt.a1[g]}, {a.gt.b0[g], a.gt.b1[g]}};
+  const int r_first = a.gt.r_begin[g], r_last = a.gt.r_begin[g + 1];  // the group's key ranges
   const bool row_tan = JVP && row >= t0;
 
   float q[E], dq[E], o[E], t[E];
@@ -59,8 +59,8 @@ __global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_simt_kernel(const
   float m = -INFINITY, l = 0.f, r = 0.f;
   const float sc = a.scale;
 
-  for (int ri = 0; ri < 2; ++ri) {
-    for (int k = rng[ri][0]; k < rng[ri][1]; ++k) {
+  for (int ri = r_first; ri < r_last; ++ri) {
+    for (int k = a.gt.k[2 * ri]; k < a.gt.k[2 * ri + 1]; ++k) {
       const bool key_tan = JVP && k >= t0;  // uniform across the wave
       float s = 0.f, ds = 0.f;
 #pragma unroll

@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <cstdio>
 #include <string>
+#include <utility>
 #include <vector>
 
 namespace attn {
@@ -14,11 +15,70 @@ bool fail(std::string* err, const std::string& msg) {
   if (err) *err = msg;
   return false;
 }
-void add_group(GroupTable* gt, int q_end, int a0, int a1, int b0, int b1) {
+
+// Open group n of the table: it owns rows up to q_end and has no key range yet.
+void begin_group(GroupTable* gt, int q_end) {
   const int g = gt->n++;
   gt->q_end[g] = q_end;
-  gt->a0[g] = a0; gt->a1[g] = a1;
-  gt->b0[g] = b0; gt->b1[g] = b1;
+  gt->r_begin[g + 1] = gt->r_begin[g];
+}
+
+// Append key range [k0, k1) (non-empty, after the group's last range and not touching
+// it) to the last group.
+bool add_range(GroupTable* gt, int k0, int k1, std::string* err) {
+  const int r = gt->r_begin[gt->n];
+  if (r == kMaxRanges)
+    return fail(err, "more than " + std::to_string(kMaxRanges) + " key ranges in all (ATTN_MAX_RANGES)");
+  gt->k[2 * r] = k0;
+  gt->k[2 * r + 1] = k1;
+  gt->r_begin[gt->n] = (uint16_t)(r + 1);
+  return true;
+}
+
+std::string at_group(int g) { return " (group " + std::to_string(g) + ")"; }
+
+// ATTN_MASK_RANGES: query-group bounds, per-group range offsets and key ranges.
+bool build_range_list(const attn_chunk_layout* layout, int L, GroupTable* gt, std::string* err) {
+  const int G = layout->num_chunks;
+  if (G < 1 || G > ATTN_MAX_GROUPS)
+    return fail(err, "number of query groups must be in [1, " + std::to_string(ATTN_MAX_GROUPS) + "], got " +
+                         std::to_string(G));
+  const int32_t* qb = layout->chunk_offsets;
+  const int32_t* ro = layout->range_offsets;
+  if (!qb) return fail(err, "chunk_offsets (the query-group bounds) is NULL");
+  if (!ro) return fail(err, "range_offsets is NULL");
+  if (qb[0] != 0) return fail(err, "the first query group must start at row 0");
+  if (ro[0] != 0) return fail(err, "range_offsets[0] must be 0");
+  for (int g = 0; g < G; ++g) {
+    if (qb[g + 1] <= qb[g]) return fail(err, "query-group bounds must be strictly increasing" + at_group(g));
+    if (ro[g + 1] < ro[g]) return fail(err, "range_offsets must not decrease" + at_group(g));
+  }
+  if (qb[G] != L)
+    return fail(err, "query groups cover " + std::to_string(qb[G]) + " rows but L = " + std::to_string(L));
+  const int32_t* rk = layout->ranges;
+  if (ro[G] > 0 && !rk) return fail(err, "ranges is NULL");
+  std::vector<std::pair<int, int>> K;
+  for (int g = 0; g < G; ++g) {
+    K.clear();
+    for (int64_t r = ro[g]; r < ro[g + 1]; ++r) {
+      const int k0 = rk[2 * r], k1 = rk[2 * r + 1];
+      if (k0 < 0 || k0 > k1 || k1 > L)
+        return fail(err, "key ranges must satisfy 0 <= begin <= end <= L" + at_group(g));
+      if (k1 > k0) K.emplace_back(k0, k1);
+    }
+    std::sort(K.begin(), K.end());
+    begin_group(gt, qb[g + 1]);
+    for (size_t i = 0; i < K.size(); ++i) {
+      if (i > 0 && K[i].first < K[i - 1].second) return fail(err, "key ranges overlap" + at_group(g));
+      const int r = gt->r_begin[gt->n];
+      if (i > 0 && K[i].first == K[i - 1].second) {
+        gt->k[2 * r - 1] = K[i].second;  // touches the previous range: extend it
+        continue;
+      }
+      if (!add_range(gt, K[i].first, K[i].second, err)) return false;
+    }
+  }
+  return true;
 }
 }  // namespace
 
@@ -26,33 +86,13 @@ bool build_groups(const attn_chunk_layout* layout, int L, GroupTable* gt, std::s
   if (!layout) return fail(err, "layout is NULL");
   if (L <= 0) return fail(err, "sequence length L must be positive, got " + std::to_string(L));
   gt->n = 0;
+  gt->r_begin[0] = 0;
   const int kind = layout->kind;
   if (kind == ATTN_MASK_FULL) {
-    add_group(gt, L, 0, L, 0, 0);
-    return true;
+    begin_group(gt, L);
+    return add_range(gt, 0, L, err);
   }
-  if (kind == ATTN_MASK_RANGES) {
-    const int G = layout->num_chunks;
-    if (G < 1 || G > ATTN_MAX_GROUPS)
-      return fail(err, "number of query groups must be in [1, " + std::to_string(ATTN_MAX_GROUPS) +
-                           "], got " + std::to_string(G));
-    const int32_t* r = layout->ranges;
-    if (!r) return fail(err, "ranges is NULL");
-    int prev = 0;
-    for (int g = 0; g < G; ++g) {
-      const int qe = r[5 * g], a0 = r[5 * g + 1], a1 = r[5 * g + 2], b0 = r[5 * g + 3], b1 = r[5 * g + 4];
-      const std::string at = " (group " + std::to_string(g) + ")";
-      if (qe <= prev) return fail(err, "query group ends must be strictly increasing" + at);
-      if (a0 < 0 || a0 > a1 || a1 > L || b0 < 0 || b0 > b1 || b1 > L)
-        return fail(err, "key ranges must satisfy 0 <= begin <= end <= L" + at);
-      if (a1 > a0 && b1 > b0 && a0 < b1 && b0 < a1) return fail(err, "key ranges overlap" + at);
-      add_group(gt, qe, a0, a1, b0, b1);
-      prev = qe;
-    }
-    if (prev != L)
-      return fail(err, "query groups cover " + std::to_string(prev) + " rows but L = " + std::to_string(L));
-    return true;
-  }
+  if (kind == ATTN_MASK_RANGES) return build_range_list(layout, L, gt, err);
   if (kind != ATTN_MASK_BLOCK_CAUSAL && kind != ATTN_MASK_TEACHER_FORCING)
     return fail(err, "unknown mask kind " + std::to_string(kind));
   const int N = layout->num_chunks;
@@ -70,56 +110,26 @@ bool build_groups(const attn_chunk_layout* layout, int L, GroupTable* gt, std::s
     if (L != half)
       return fail(err, "block-causal layout covers " + std::to_string(half) + " tokens but L = " +
                            std::to_string(L));
-    for (int j = 0; j < N; ++j) add_group(gt, o[j + 1], 0, o[j + 1], 0, 0);
+    for (int j = 0; j < N; ++j) {
+      begin_group(gt, o[j + 1]);
+      add_range(gt, 0, o[j + 1], err);
+    }
     return true;
   }
   if ((int64_t)L != 2 * (int64_t)half)
     return fail(err, "teacher-forcing layout needs L = 2 * chunk_offsets[N] = " +
                          std::to_string(2 * (int64_t)half) + ", got L = " + std::to_string(L));
-  // clean chunk j: clean chunks <= j
-  for (int j = 0; j < N; ++j) add_group(gt, o[j + 1], 0, o[j + 1], 0, 0);
-  // noisy chunk i: clean chunks < i, then its own noisy chunk
-  for (int i = 0; i < N; ++i) add_group(gt, half + o[i + 1], 0, o[i], half + o[i], half + o[i + 1]);
-  return true;
-}
-
-bool transpose_groups(const GroupTable& gt, int L, GroupTable* kt, std::string* err) {
-  // key breakpoints: every range end point; between two of them the admitting groups are fixed
-  std::vector<int> cuts = {0, L};
-  for (int g = 0; g < gt.n; ++g) {
-    if (gt.a1[g] > gt.a0[g]) { cuts.push_back(gt.a0[g]); cuts.push_back(gt.a1[g]); }
-    if (gt.b1[g] > gt.b0[g]) { cuts.push_back(gt.b0[g]); cuts.push_back(gt.b1[g]); }
+  // clean chunk j: clean chunks <= j (N ranges)
+  for (int j = 0; j < N; ++j) {
+    begin_group(gt, o[j + 1]);
+    add_range(gt, 0, o[j + 1], err);
   }
-  std::sort(cuts.begin(), cuts.end());
-  cuts.erase(std::unique(cuts.begin(), cuts.end()), cuts.end());
-  kt->n = 0;
-  for (size_t c = 0; c + 1 < cuts.size(); ++c) {
-    const int k = cuts[c];  // representative key of [cuts[c], cuts[c+1])
-    int runs[2][2] = {{0, 0}, {0, 0}};
-    int nr = 0;
-    for (int g = 0; g < gt.n; ++g) {
-      const bool hit = (k >= gt.a0[g] && k < gt.a1[g]) || (k >= gt.b0[g] && k < gt.b1[g]);
-      if (!hit) continue;
-      const int q0 = group_q_begin(gt, g), q1 = gt.q_end[g];
-      if (nr > 0 && runs[nr - 1][1] == q0) {
-        runs[nr - 1][1] = q1;  // adjacent query groups form one run
-        continue;
-      }
-      if (nr == 2)
-        return fail(err, "the transposed mask needs more than two query ranges for key " + std::to_string(k));
-      runs[nr][0] = q0; runs[nr][1] = q1;
-      ++nr;
-    }
-    const int e = cuts[c + 1];
-    const int n = kt->n;
-    if (n > 0 && kt->a0[n - 1] == runs[0][0] && kt->a1[n - 1] == runs[0][1] && kt->b0[n - 1] == runs[1][0] &&
-        kt->b1[n - 1] == runs[1][1]) {
-      kt->q_end[n - 1] = e;  // same query ranges as the previous key interval: extend it
-      continue;
-    }
-    if (n == kMaxGroups)
-      return fail(err, "the transposed mask needs more than " + std::to_string(kMaxGroups) + " key groups");
-    add_group(kt, e, runs[0][0], runs[0][1], runs[1][0], runs[1][1]);
+  // noisy chunk i: clean chunks < i, then its own noisy chunk (2N - 1 ranges; 3N - 1 <=
+  // kMaxRanges for N <= ATTN_MAX_CHUNKS)
+  for (int i = 0; i < N; ++i) {
+    begin_group(gt, half + o[i + 1]);
+    if (i > 0) add_range(gt, 0, o[i], err);
+    add_range(gt, half + o[i], half + o[i + 1], err);
   }
   return true;
 }
@@ -128,7 +138,9 @@ int64_t count_pairs(const GroupTable& gt) {
   int64_t total = 0;
   for (int g = 0; g < gt.n; ++g) {
     const int64_t rows = gt.q_end[g] - group_q_begin(gt, g);
-    total += rows * ((int64_t)(gt.a1[g] - gt.a0[g]) + (gt.b1[g] - gt.b0[g]));
+    int64_t keys = 0;
+    for (int r = gt.r_begin[g]; r < gt.r_begin[g + 1]; ++r) keys += gt.k[2 * r + 1] - gt.k[2 * r];
+    total += rows * keys;
   }
   return total;
 }

@@ -11,15 +11,9 @@
 namespace attn {
 
 // Validate `layout` against the sequence length L and derive its query-group
-// table.  Returns false and fills *err on an invalid layout.
+// table (ranges of each group sorted, empty ones dropped, touching ones merged).
+// Returns false and fills *err on an invalid layout.
 bool build_groups(const attn_chunk_layout* layout, int L, GroupTable* gt, std::string* err);
-
-// The mask with the roles of queries and keys swapped, in the same table form: key
-// group g owns keys [q_end(g-1), q_end(g)) and is admitted by the queries in [a0, a1)
-// and [b0, b1).  Fails (with a message) if some key needs more than two query ranges
-// or more than kMaxGroups key groups arise; never for the full, block-causal and
-// teacher-forcing layouts.
-bool transpose_groups(const GroupTable& gt, int L, GroupTable* kt, std::string* err);
 
 // Admissible (query, key) pairs of the mask, one (batch, head).
 int64_t count_pairs(const GroupTable& gt);

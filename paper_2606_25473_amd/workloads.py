@@ -33,7 +33,9 @@ class Workload:
     D: int
     dtype: str                 # "f32" or "bf16"
     kind: str                  # MASK_* above
-    offsets: tuple = field(default=())   # chunk prefix offsets (TF / block-causal) or query groups (ranges)
+    # chunk prefix offsets (TF / block-causal), or query groups ((q0, q1, ((k0, k1), ...)), ...)
+    # tiling [0, L) (ranges)
+    offsets: tuple = field(default=())
     L_full: int = 0            # sequence length for the full mask
     tangent_std: float = 1.0
 
@@ -42,7 +44,7 @@ class Workload:
         if self.kind == MASK_FULL:
             return self.L_full
         if self.kind == MASK_RANGES:
-            return self.offsets[-1][0]
+            return self.offsets[-1][1]
         half = self.offsets[-1]
         return 2 * half if self.kind == MASK_TEACHER_FORCING else half
 
@@ -116,6 +118,7 @@ def custom_workload(name, B, H, D, dtype, kind, num_chunks=0, chunk=0, L=0, tang
     if kind == MASK_FULL:
         return Workload(name, B, H, D, dtype, kind, (), L, tangent_std)
     if kind == MASK_RANGES:
-        return Workload(name, B, H, D, dtype, kind, tuple(tuple(g) for g in offsets), 0, tangent_std)
+        groups = tuple((int(q0), int(q1), tuple((int(a), int(b)) for a, b in ks)) for q0, q1, ks in offsets)
+        return Workload(name, B, H, D, dtype, kind, groups, 0, tangent_std)
     offs = tuple(offsets) if offsets is not None else uniform_offsets(num_chunks, chunk)
     return Workload(name, B, H, D, dtype, kind, offs, 0, tangent_std)

@@ -44,7 +44,7 @@ def _np(t):
 
 
 def _offsets(w):
-    return [tuple(g) for g in w.offsets] if w.kind == MASK_RANGES else (list(w.offsets) if w.offsets else None)
+    return list(w.offsets) if w.kind == MASK_RANGES else (list(w.offsets) if w.offsets else None)
 
 
 def _inputs(w, seed):
@@ -78,10 +78,21 @@ SHAPES = [
     custom_workload("bwd_full_d64_f32", 1, 2, 64, "f32", MASK_FULL, L=50),
     # rows 100..149 see no key; keys 450..499 are seen by no row
     custom_workload("bwd_ranges_bf16", 1, 2, 128, "bf16", MASK_RANGES,
-                    offsets=[(100, 0, 100, 300, 350), (150, 0, 0, 0, 0), (400, 0, 450, 0, 0),
-                             (500, 100, 200, 0, 0)], tangent_std=0.5),
+                    offsets=[(0, 100, [(0, 100), (300, 350)]), (100, 150, []), (150, 400, [(0, 450)]),
+                             (400, 500, [(100, 200)])], tangent_std=0.5),
     custom_workload("bwd_ranges_f32", 1, 1, 64, "f32", MASK_RANGES,
-                    offsets=[(10, 0, 10, 30, 35), (15, 0, 0, 0, 0), (40, 0, 20, 0, 0)]),
+                    offsets=[(0, 10, [(0, 10), (30, 35)]), (10, 15, []), (15, 40, [(0, 20)])]),
+    # several key ranges per group (touching, out of order), a group admitted by keys that
+    # three separate query runs see
+    custom_workload("bwd_ranges_many_bf16", 1, 2, 128, "bf16", MASK_RANGES,
+                    offsets=[(0, 300, [(0, 40), (100, 101), (500, 700), (900, 1000)]), (300, 333, []),
+                             (333, 700, [(950, 1000), (0, 40), (40, 80), (600, 650)]),
+                             (700, 1000, [(0, 1), (200, 260), (690, 1000)])], tangent_std=0.5),
+    custom_workload("bwd_ranges_many_d64_bf16", 1, 2, 64, "bf16", MASK_RANGES,
+                    offsets=[(0, 64, [(0, 10), (64, 65), (128, 130)]), (64, 128, [(0, 10)]),
+                             (128, 200, [(0, 10), (120, 200)])], tangent_std=0.5),
+    custom_workload("bwd_ranges_many_f32", 1, 1, 128, "f32", MASK_RANGES,
+                    offsets=[(0, 20, [(0, 3), (5, 8), (30, 40)]), (20, 30, [(0, 3)]), (30, 60, [(0, 60)])]),
 ]
 
 
@@ -109,8 +120,8 @@ def test_backward_vs_oracle(w):
     if w.kind == MASK_RANGES:
         # fully masked rows and unseen keys get exactly zero
         m = np.zeros(w.L, dtype=bool)
-        for q0g, q1g, grp in zip([0] + [g[0] for g in w.offsets[:-1]], [g[0] for g in w.offsets], w.offsets):
-            if grp[1] == grp[2] and grp[3] == grp[4]:
+        for q0g, q1g, ks in w.offsets:
+            if all(k1 == k0 for k0, k1 in ks):
                 m[q0g:q1g] = True
         assert (gq[:, :, torch.from_numpy(np.flatnonzero(m)).cuda()] == 0).all()
         unseen = np.flatnonzero(~np.abs(ref[2]).sum(axis=(0, 1, 3)).astype(bool))

@@ -27,7 +27,7 @@ pytestmark = pytest.mark.gpu
 
 L, D, W, G = 1 << 24, 128, 256, 64
 R = L // G
-GROUPS = [((g + 1) * R, 0, W, L - W * (g + 1), L - W * g) for g in range(G)]
+GROUPS = [(g * R, (g + 1) * R, [(0, W), (L - W * (g + 1), L - W * g)]) for g in range(G)]
 
 
 def _say(msg):
@@ -76,7 +76,7 @@ def test_largest_head_jvp_forward_backward():
     assert w.L == L and L * D == 1 << 31
     _say(f"[max-size] L = 2^24, D = 128 (4 GiB per bf16 tensor), {G} query groups: generating inputs on the GPU")
     x = make_inputs(w, "cuda", 51)
-    groups = [tuple(g) for g in GROUPS]
+    groups = list(GROUPS)
     o, do, lse = attn_jvp_fwd(x["Q"], x["K"], x["V"], x["dQ"], x["dK"], x["dV"], w.kind, groups)
     of, lsef = attn_fwd(x["Q"], x["K"], x["V"], w.kind, groups)
     torch.cuda.synchronize()

@@ -254,17 +254,33 @@ def test_full_mask_growing_scores():
 
 # ----------------------------------------------------------------------------- explicit range lists
 
-def _random_ranges(L, G, seed):
+def _random_ranges(L, G, seed, max_ranges=5):
+    """Seeded query groups tiling [0, L), each with 0..max_ranges disjoint key ranges in
+    random order (some empty, some touching)."""
     rng = np.random.default_rng(seed)
-    cuts = np.sort(rng.choice(np.arange(1, L), size=G - 1, replace=False))
+    cuts = [0] + sorted(int(c) for c in rng.choice(np.arange(1, L), size=G - 1, replace=False)) + [L]
     groups = []
-    for e in list(cuts) + [L]:
-        a0, a1, b0, b1 = (int(v) for v in np.sort(rng.integers(0, L + 1, size=4)))
-        if rng.random() < 0.15:
-            a1 = a0
-        if rng.random() < 0.3:
-            b1 = b0
-        groups.append((int(e), a0, a1, b0, b1))
+    for q0, q1 in zip(cuts, cuts[1:]):
+        n = int(rng.integers(0, max_ranges + 1))
+        pts = sorted(int(v) for v in rng.integers(0, L + 1, size=2 * n))
+        ks = [(pts[2 * i], pts[2 * i + 1]) for i in range(n)]
+        if n >= 2 and rng.random() < 0.3:
+            ks[1] = (ks[0][1], max(ks[0][1], ks[1][1]))
+        rng.shuffle(ks)
+        groups.append((q0, q1, [tuple(k) for k in ks]))
+    return groups
+
+
+def _striped(L, G, stripes, width, seed):
+    """Groups of L/G rows, each admitting `stripes` narrow key ranges spread over the whole
+    sequence: more separate block runs per query tile than a tile plan holds, so the plan
+    merges runs and masks the blocks in between."""
+    rng = np.random.default_rng(seed)
+    groups = []
+    bounds = [round(i * L / G) for i in range(G + 1)]
+    for q0, q1 in zip(bounds, bounds[1:]):
+        starts = sorted(int(v) for v in rng.choice(np.arange(0, L - width, 2 * width), size=stripes, replace=False))
+        groups.append((q0, q1, [(a, a + int(rng.integers(1, width + 1))) for a in starts]))
     return groups
 
 
@@ -285,13 +301,26 @@ def _check_ranges(w, seed):
 
 @pytest.mark.parametrize("dt,D,L,G,seed", [("bf16", 128, 700, 9, 1), ("bf16", 128, 1500, 40, 2),
                                            ("bf16", 64, 333, 5, 3), ("f32", 128, 200, 6, 4),
-                                           ("f32", 64, 97, 12, 5)])
+                                           ("f32", 64, 97, 12, 5), ("bf16", 128, 2100, 25, 6),
+                                           ("bf16", 64, 900, 60, 7), ("f32", 128, 300, 30, 8)])
 def test_random_range_lists(dt, D, L, G, seed):
     groups = _random_ranges(L, G, seed)
     if seed == 1:
-        groups[0] = (groups[0][0], 0, 0, 0, 0)  # guarantee a fully masked group
+        groups[0] = (groups[0][0], groups[0][1], [])  # guarantee a fully masked group
+    if seed == 6:
+        groups[1] = (groups[1][0], groups[1][1], [(0, 5), (40, 41), (300, 700), (900, 901), (2000, 2100)])
     w = custom_workload(f"ranges_{dt}_{D}_{L}_{G}", 1, 2, D, dt, "ranges", offsets=groups, tangent_std=0.5)
     _say(f"[ranges] {w.name} groups={groups[:3]}...")
+    _check_ranges(w, seed)
+
+
+@pytest.mark.parametrize("dt,D,L,G,stripes,seed", [("bf16", 128, 3000, 6, 9, 21), ("bf16", 64, 1200, 3, 12, 22),
+                                                    ("f32", 128, 700, 4, 7, 23)])
+def test_range_lists_with_more_runs_than_a_tile_plan_holds(dt, D, L, G, stripes, seed):
+    groups = _striped(L, G, stripes, 40, seed)
+    w = custom_workload(f"stripes_{dt}_{D}_{L}_{G}x{stripes}", 1, 2, D, dt, "ranges", offsets=groups,
+                        tangent_std=0.5)
+    _say(f"[ranges] {w.name} group 0 ranges={groups[0][2]}")
     _check_ranges(w, seed)
 
 
@@ -300,8 +329,8 @@ def test_ranges_equal_to_tf_layout_match_tf_bitwise():
     outputs are bit-identical to the teacher-forcing layout."""
     N, C = 3, 100
     half = N * C
-    groups = [((j + 1) * C, 0, (j + 1) * C, 0, 0) for j in range(N)]
-    groups += [(half + (i + 1) * C, 0, i * C, half + i * C, half + (i + 1) * C) for i in range(N)]
+    groups = [(j * C, (j + 1) * C, [(0, (j + 1) * C)]) for j in range(N)]
+    groups += [(half + i * C, half + (i + 1) * C, [(0, i * C), (half + i * C, half + (i + 1) * C)]) for i in range(N)]
     w_tf = custom_workload("tf_as_tf", 1, 2, 128, "bf16", MASK_TEACHER_FORCING, N, C, tangent_std=0.5)
     w_rg = custom_workload("tf_as_ranges", 1, 2, 128, "bf16", "ranges", offsets=groups, tangent_std=0.5)
     _say("[ranges] TF table vs TF layout")

@@ -27,25 +27,30 @@ LAYOUTS = [
     (MASK_BLOCK_CAUSAL, [0, 50, 77, 200, 333], 333),
     (MASK_FULL, None, 1000),
     (MASK_FULL, None, 7),
-    (MASK_RANGES, [(100, 0, 0, 0, 0), (300, 0, 50, 250, 300), (301, 0, 301, 0, 0), (520, 400, 520, 10, 20)], 520),
-    (MASK_RANGES, [(7, 3, 5, 0, 0)], 7),
+    (MASK_RANGES, [(0, 100, []), (100, 300, [(0, 50), (250, 300)]), (300, 301, [(0, 301)]),
+                   (301, 520, [(400, 520), (10, 20)])], 520),
+    (MASK_RANGES, [(0, 7, [(3, 5)])], 7),
+    # several key ranges per group, adjacent ones, an empty one, out of order
+    (MASK_RANGES, [(0, 40, [(0, 5), (30, 33), (60, 90), (100, 101)]), (40, 41, []),
+                   (41, 200, [(10, 20), (20, 40), (150, 200)]), (200, 300, [(299, 300), (0, 1), (50, 50), (120, 180)])],
+     300),
 ]
 
 
-def random_ranges(L, G, seed):
-    """Seeded random query groups with two non-overlapping key ranges (some empty)."""
+def random_ranges(L, G, seed, max_ranges=5):
+    """Seeded random query groups tiling [0, L), each with 0..max_ranges disjoint key ranges
+    (some empty, some touching, in random order)."""
     rng = np.random.default_rng(seed)
-    cuts = np.sort(rng.choice(np.arange(1, L), size=G - 1, replace=False))
-    ends = list(cuts) + [L]
+    cuts = [0] + sorted(int(c) for c in rng.choice(np.arange(1, L), size=G - 1, replace=False)) + [L]
     groups = []
-    for e in ends:
-        p = np.sort(rng.integers(0, L + 1, size=4))
-        a0, a1, b0, b1 = (int(v) for v in p)
-        if rng.random() < 0.15:
-            a1 = a0
-        if rng.random() < 0.3:
-            b1 = b0
-        groups.append((int(e), a0, a1, b0, b1))
+    for q0, q1 in zip(cuts, cuts[1:]):
+        n = int(rng.integers(0, max_ranges + 1))
+        pts = sorted(int(v) for v in rng.integers(0, L + 1, size=2 * n))
+        ks = [(pts[2 * i], pts[2 * i + 1]) for i in range(n)]
+        if n >= 2 and rng.random() < 0.3:  # make two neighbours touch
+            ks[1] = (ks[0][1], max(ks[0][1], ks[1][1]))
+        rng.shuffle(ks)
+        groups.append((q0, q1, [tuple(k) for k in ks]))
     return groups
 
 
@@ -84,59 +89,74 @@ def test_workload_pair_counts_closed_form(lib, name):
         assert n == C * C * N * (N + 1)
 
 
+def _table_mask(groups, L):
+    """Mask of a library table [(q0, q1, [(k0, k1), ...]), ...], checking its normal form:
+    the groups tile [0, L); each group's ranges are non-empty, increasing, not touching."""
+    m = np.zeros((L, L), dtype=bool)
+    prev = 0
+    for q0, q1, ks in groups:
+        assert q0 == prev and q1 > q0
+        prev = q1
+        for (a0, a1), (b0, b1) in zip(ks, ks[1:]):
+            assert a1 < b0
+        for k0, k1 in ks:
+            assert 0 <= k0 < k1 <= L
+            m[q0:q1, k0:k1] = True
+    assert prev == L
+    return m
+
+
 @pytest.mark.parametrize("kind,offsets,L", LAYOUTS)
 def test_query_groups_reproduce_mask(lib, kind, offsets, L):
     groups = binding.query_groups(kind, offsets, L)
-    m = np.zeros((L, L), dtype=bool)
-    prev = 0
-    for q0, q1, a0, a1, b0, b1 in groups:
-        assert q0 == prev and q1 > q0
-        prev = q1
-        m[q0:q1, a0:a1] = True
-        m[q0:q1, b0:b1] = True
-    assert prev == L
-    assert np.array_equal(m, allowed_mask(kind, offsets, L))
+    assert np.array_equal(_table_mask(groups, L), allowed_mask(kind, offsets, L))
 
 
 @pytest.mark.parametrize("kind,offsets,L", LAYOUTS)
-def test_key_groups_reproduce_transposed_mask(lib, kind, offsets, L):
-    """The key-group table of the backward's key-side pass is the mask transposed."""
-    groups = binding.key_groups(kind, offsets, L)
-    mt = np.zeros((L, L), dtype=bool)   # mt[key, query]
-    prev = 0
-    for k0, k1, a0, a1, b0, b1 in groups:
-        assert k0 == prev and k1 > k0
-        prev = k1
-        assert a0 <= a1 and b0 <= b1 and (a1 <= b0 or b1 == b0)
-        mt[k0:k1, a0:a1] = True
-        mt[k0:k1, b0:b1] = True
-    assert prev == L
-    assert np.array_equal(mt, allowed_mask(kind, offsets, L).T)
+def test_key_tile_plans_cover_transposed_mask(lib, kind, offsets, L):
+    """The backward's key tiles visit every query block with an admissible pair, once, in
+    order, and skip the mask only on blocks where every (query, key) pair is admissible."""
+    KT, QB = 128, 64
+    mask = allowed_mask(kind, offsets, L)
+    for t in range((L + KT - 1) // KT):
+        keys = slice(t * KT, min(L, t * KT + KT))
+        plan = binding.key_tile_plan(kind, offsets, L, t)
+        blocks = [b for b, _ in plan]
+        assert blocks == sorted(set(blocks))
+        visited = np.zeros(L, dtype=bool)
+        for b, full in plan:
+            visited[b * QB:(b + 1) * QB] = True
+            if full:
+                assert b * QB + QB <= L and mask[b * QB:b * QB + QB, keys].all()
+        assert not (mask[:, keys] & ~visited[:, None]).any()
 
 
-def test_key_groups_of_teacher_forcing_closed_form(lib):
-    # clean chunk j is seen by the clean queries from chunk j on and the noisy queries
-    # of later chunks; noisy chunk i by its own noisy queries only
-    offs = [0, 3, 7, 10]
-    assert binding.key_groups("teacher_forcing", offs, 20) == [
-        (0, 3, 0, 10, 13, 20), (3, 7, 3, 10, 17, 20), (7, 10, 7, 10, 0, 0),
-        (10, 13, 10, 13, 0, 0), (13, 17, 13, 17, 0, 0), (17, 20, 17, 20, 0, 0)]
+def test_key_tile_plan_of_teacher_forcing(lib):
+    # keys 0..127 of 4 chunks x 64 tokens: clean chunks 0 and 1, seen by clean rows 0..255
+    # (all of them admit every key of the tile from row 64 on) and noisy rows 320..511
+    plan = binding.key_tile_plan("teacher_forcing", [0, 64, 128, 192, 256], 512, 0)
+    assert [b for b, _ in plan] == [0, 1, 2, 3, 5, 6, 7]
+    assert [f for _, f in plan] == [False, True, True, True, False, True, True]
 
 
-def test_key_groups_reject_three_query_ranges(lib):
-    # key 0 is admitted by groups 0, 2 and 4, which are not adjacent: three query runs
-    groups = [(2, 0, 1, 0, 0), (4, 1, 2, 0, 0), (6, 0, 1, 0, 0), (8, 1, 2, 0, 0), (10, 0, 1, 0, 0)]
-    with pytest.raises(binding.AttnError):
-        binding.key_groups("ranges", groups, 10)
-    assert "two query ranges" in binding.last_error()
+def _many_runs():
+    """128 two-row query groups; group g admits keys g and 128 + g: each key is seen by one
+    group, and a key tile by 128 separate query runs."""
+    return [(2 * g, 2 * g + 2, [(g, g + 1), (128 + g, 129 + g)]) for g in range(128)]
 
 
-@pytest.mark.parametrize("seed", range(6))
+def test_key_tile_plan_with_many_query_runs(lib):
+    test_key_tile_plans_cover_transposed_mask(lib, MASK_RANGES, _many_runs(), 256)
+    assert len(binding.query_groups("ranges", _many_runs(), 256)) == 128
+
+
+@pytest.mark.parametrize("seed", range(10))
 def test_random_range_lists(lib, seed):
     L = int(np.random.default_rng(seed).integers(40, 900))
-    groups = random_ranges(L, 1 + seed * 7, seed)
+    groups = random_ranges(L, 1 + seed * 5, seed)
     assert binding.count_unmasked_pairs("ranges", groups, L) == count_allowed_pairs(MASK_RANGES, groups, L)
     test_query_groups_reproduce_mask(lib, MASK_RANGES, groups, L)
+    test_key_tile_plans_cover_transposed_mask(lib, MASK_RANGES, groups, L)
     test_tile_plans_cover_mask_and_full_blocks_are_full(lib, MASK_RANGES, groups, L)
 
 
@@ -231,6 +251,14 @@ def _with(i, value):
     return p
 
 
+def _raw(bounds, roffs, flat):
+    """An ATTN_MASK_RANGES layout built directly from its three arrays (no binding checks)."""
+    arrs = [None if a is None else (ctypes.c_int32 * max(1, len(a)))(*a) for a in (bounds, roffs, flat)]
+    lay = binding._Layout(3, len(bounds) - 1, *arrs)
+    lay._keep = arrs
+    return lay
+
+
 def _call(lib, **kw):
     dtype, B, H, L, D = kw.get("dtype", 1), kw.get("B", 1), kw.get("H", 1), kw.get("L", 64), kw.get("D", 64)
     es = 4 if dtype == 0 else 2
@@ -256,11 +284,22 @@ def _call(lib, **kw):
     (dict(layout=make_layout("block_causal", [0, 10, 20]), L=64), 1, "block-causal"),
     (dict(layout=make_layout("teacher_forcing", list(range(66))), L=130), 1, "num_chunks"),
     (dict(layout=make_layout(9)), 1, "kind"),
-    (dict(layout=make_layout("ranges", [(30, 0, 10, 5, 20), (64, 0, 64, 0, 0)])), 1, "overlap"),
-    (dict(layout=make_layout("ranges", [(30, 0, 10, 0, 0), (60, 0, 64, 0, 0)])), 1, "cover"),
-    (dict(layout=make_layout("ranges", [(30, 0, 10, 0, 0), (30, 0, 64, 0, 0)])), 1, "increasing"),
-    (dict(layout=make_layout("ranges", [(64, 0, 65, 0, 0)])), 1, "begin <= end <= L"),
-    (dict(layout=make_layout("ranges", [])), 1, "query groups"),
+    (dict(layout=_raw([0, 30, 64], [0, 2, 3], [0, 10, 5, 20, 0, 64])), 1, "overlap"),
+    (dict(layout=_raw([0, 30, 60], [0, 1, 2], [0, 10, 0, 64])), 1, "cover"),
+    (dict(layout=_raw([0, 30, 30, 64], [0, 1, 1, 2], [0, 10, 0, 64])), 1, "increasing"),
+    (dict(layout=_raw([5, 64], [0, 1], [0, 10])), 1, "row 0"),
+    (dict(layout=_raw([0, 64], [0, 1], [0, 65])), 1, "begin <= end <= L"),
+    (dict(layout=_raw([0, 64], [0, 1], [9, 3])), 1, "begin <= end <= L"),
+    (dict(layout=_raw([0, 32, 64], [0, 2, 1], [0, 1, 2, 3])), 1, "must not decrease"),
+    (dict(layout=_raw([0, 64], [1, 1], [0, 1])), 1, "range_offsets[0]"),
+    (dict(layout=_raw([0, 64], None, [0, 1])), 1, "range_offsets is NULL"),
+    (dict(layout=_raw([0, 64], [0, 1], None)), 1, "ranges is NULL"),
+    (dict(layout=_raw([0], [0], [])), 1, "query groups"),
+    (dict(layout=_raw(list(range(0, 130)), list(range(130)), list(range(2 * 129))), L=129), 1,
+     "query groups"),
+    # 257 disjoint, non-touching ranges in one group: more than the table holds
+    (dict(layout=_raw([0, 1024], [0, 257], [v for i in range(257) for v in (3 * i, 3 * i + 1)]), L=1024), 1,
+     "ATTN_MAX_RANGES"),
     # size limits: 32-bit offsets within a bf16 head, work-groups per launch, fp32 grid rows
     (dict(L=(1 << 24) + 2, D=128, layout=make_layout("teacher_forcing", [0, (1 << 23) + 1])), 1, "2^31"),
     (dict(L=(1 << 25) + 2, D=64, layout=make_layout("teacher_forcing", [0, (1 << 24) + 1])), 1, "2^31"),
@@ -315,8 +354,7 @@ def test_backward_entry_point_validates(lib):
     q = list(p); q[7] = q[6] + 1024
     assert call(q) == 1 and "overlap" in binding.last_error()
     assert call(p, D=80) == 2 and "head_dim" in binding.last_error()
-    three = [(8, 0, 1, 0, 0), (16, 1, 2, 0, 0), (24, 0, 1, 0, 0), (32, 1, 2, 0, 0), (64, 0, 1, 0, 0)]
-    assert call(p, layout=make_layout("ranges", three)) == 2 and "two query ranges" in binding.last_error()
+    assert call(p, layout=make_layout("teacher_forcing", [0, 16, 40])) == 1 and "L = 2" in binding.last_error()
 
 
 @_no_gpu
