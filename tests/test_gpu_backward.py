@@ -153,29 +153,46 @@ def test_backward_deterministic():
         assert torch.equal(u, t)
 
 
-def test_backward_full_size_sampled():
-    """Wan2.1-1.3B chunk-wise TF (B=1, H=12, L=65520, D=128, bf16), HIP forward then
-    backward in the launch configuration the bench times; sampled rows of gQ and Delta
-    and sampled keys of gK, gV against the oracle."""
-    w = WORKLOADS["wan1.3b_chunkwise_tf"]
-    _say(f"[backward] full size {w.name}: generating inputs on the GPU")
+def _cheap_keys(w, rng):
+    """Keys whose gradients the oracle can form from few query rows: for teacher forcing,
+    the last clean chunk (seen by its own clean rows only) and the first noisy chunk (seen
+    by its own noisy rows, which admit no other key); for the full mask any key (every row
+    sees it, so the oracle runs the whole head once)."""
+    L = w.L
+    if w.kind == MASK_FULL:
+        return np.unique(np.concatenate([[0, L // 2, L - 1], rng.integers(0, L, 9)]))
+    offs = list(w.offsets)
+    half = L // 2
+    pools = [np.arange(offs[-2], half), half + np.arange(offs[0], offs[1])]
+    return np.unique(np.concatenate([[offs[-2], half - 1, half, half + offs[1] - 1]] +
+                                    [rng.choice(p, 6) for p in pools]))
+
+
+@pytest.mark.parametrize("name,heads", [("wan1.3b_chunkwise_tf", ((0, 0), (0, 11))),
+                                        ("wan1.3b_framewise_tf", ((0, 5),)),
+                                        ("wan1.3b_bidirectional", ((0, 7),)),
+                                        ("wan14b_chunkwise_tf", ((0, 3), (1, 39)))])
+def test_backward_full_size_sampled(name, heads):
+    """The Wan-shaped workloads (bf16, D = 128) in the launch configuration the bench
+    times: HIP forward, then backward; sampled rows of gQ and Delta (tile and chunk
+    boundaries included) and sampled keys of gK, gV against the oracle."""
+    w = WORKLOADS[name]
+    _say(f"[backward] full size {w.name} B={w.B} H={w.H} L={w.L}: generating inputs on the GPU")
     x = make_inputs(w, "cuda", 0)
     q, k, v, go = x["Q"], x["K"], x["V"], x["dV"]
-    offs = list(w.offsets)
+    offs = list(w.offsets) if w.offsets else None
     o, lse = attn_fwd(q, k, v, w.kind, offs)
     gq, gk, gv, delta = attn_bwd(q, k, v, o, go, lse, w.kind, offs)
     torch.cuda.synchronize()
     _say("[backward] full size: kernels done, checking sampled rows and keys")
     for t in (gq, gk, gv, delta):
         assert torch.isfinite(t).all()
-    half = w.L // 2
     rng = np.random.default_rng(0)
-    rows = np.unique(np.concatenate([[0, half - 1, half, w.L - 1], rng.integers(0, w.L, 20)]))
-    # keys of the last clean chunk and of the first two noisy chunks: each is seen by few
-    # query rows with few keys, which keeps the oracle's work small (~20 s)
-    pools = [np.arange(offs[-2], half), half + np.arange(offs[0], offs[2])]
-    keys = np.unique(np.concatenate([[offs[-2], half - 1, half]] + [rng.choice(p, 6) for p in pools]))
-    for b, h in ((0, w.H - 1),):
+    half = w.L // 2
+    rows = np.unique(np.concatenate([[0, half - 1, half, w.L - 1], np.arange(0, w.L, 256 * 16),
+                                     np.arange(255, w.L, 256 * 16), rng.integers(0, w.L, 16)]))
+    keys = _cheap_keys(w, rng)
+    for b, h in heads:
         sl = [_np(t[b:b + 1, h:h + 1]) for t in (q, k, v, go)]
         rq, rk, rv, rd = attention_vjp(*sl, w.kind, offs, rows=rows, keys=keys)
         ri, ki = torch.from_numpy(rows).cuda(), torch.from_numpy(keys).cuda()

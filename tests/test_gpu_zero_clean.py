@@ -132,12 +132,15 @@ def test_zero_clean_deterministic():
         assert torch.equal(u, v)
 
 
-def test_zero_clean_full_size_headline():
-    """Wan2.1-1.3B chunk-wise TF (B=1, H=12, L=65520, D=128, bf16) in the launch
-    configuration the bench times: equal to the dense kernel on zero-padded tangents,
-    and sampled rows of both halves against the oracle."""
-    w = WORKLOADS["wan1.3b_chunkwise_tf"]
-    _say(f"[zero-clean] full size {w.name}: generating inputs on the GPU")
+@pytest.mark.parametrize("name,nheads", [("wan1.3b_chunkwise_tf", 4), ("wan1.3b_framewise_tf", 4),
+                                         ("wan14b_chunkwise_tf", 8)])
+def test_zero_clean_full_size(name, nheads):
+    """The Wan-shaped workloads (L = 65520, D = 128, bf16) in the launch configuration the
+    bench times: equal to the dense kernel on zero-padded tangents over the whole tensors,
+    and sampled rows of both halves (every tile boundary and chunk boundary) of spread
+    heads against the oracle."""
+    w = WORKLOADS[name]
+    _say(f"[zero-clean] full size {w.name} B={w.B} H={w.H}: generating inputs on the GPU")
     x = make_inputs(w, "cuda", 0)
     g = _noisy(x)
     o, don, lse = attn_jvp_fwd_zero_clean(*g, list(w.offsets))
@@ -145,14 +148,18 @@ def test_zero_clean_full_size_headline():
     _say("[zero-clean] full size: kernel done, comparing with the dense kernel")
     assert torch.isfinite(o).all() and torch.isfinite(don).all() and torch.isfinite(lse).all()
     _check_dense_equal(w, x, o, don, lse)
+    del x
     half = w.L // 2
     rows = sorted({0, half - 1, half, half + 1, w.L - 1} |
+                  {t for t in range(0, w.L, 128)} | {min(w.L, t + 128) - 1 for t in range(0, w.L, 128)} |
                   {half + o_ + d for o_ in w.offsets[1:-1] for d in (-1, 0)} |
                   {o_ + d for o_ in w.offsets[1:-1] for d in (-1, 0)} |
                   set(int(r) for r in np.random.default_rng(0).integers(0, w.L, 16)))
     rows = np.array(rows)
     ridx = torch.from_numpy(rows).cuda()
-    for b, h in ((0, 0), (0, w.H - 1)):
+    pairs = [(b, h) for b in range(w.B) for h in range(w.H)]
+    heads = [pairs[i] for i in np.unique(np.linspace(0, len(pairs) - 1, nheads).round().astype(int))]
+    for b, h in heads:
         sl = [_np(t[b:b + 1, h:h + 1]) for t in g]
         O, dO, LSE = attention_jvp_zero_clean(*sl, list(w.offsets), rows=rows)
         noisy = rows >= half

@@ -422,3 +422,22 @@ def test_schedule_helpers_on_the_host(tmp_path):
                     os.path.join(root, "tests", "c", "schedule_check.cpp"), "-o", exe], check=True)
     out = subprocess.run([exe], capture_output=True, text=True)
     assert out.returncode == 0 and out.stdout.strip() == "OK", out.stdout + out.stderr
+
+
+def test_binding_checks_caller_supplied_outputs():
+    """Outputs passed in `out` must have the shape, dtype, device and layout the call
+    writes; the check runs before any library call (here on CPU tensors, q's device)."""
+    import torch
+    q = torch.zeros(1, 2, 8, 64, dtype=torch.bfloat16)
+    good = [("O", q.shape, q.dtype), ("LSE", (1, 2, 8), torch.float32)]
+    binding._check_outs([torch.empty_like(q), torch.empty(1, 2, 8)], good, q)
+    bad_sets = [
+        [torch.empty(1, 2, 7, 64, dtype=torch.bfloat16), torch.empty(1, 2, 8)],   # short O
+        [torch.empty_like(q, dtype=torch.float32), torch.empty(1, 2, 8)],         # O dtype
+        [torch.empty_like(q), torch.empty(1, 2, 8, dtype=torch.bfloat16)],        # LSE dtype
+        [torch.empty_like(q), torch.empty(1, 2, 16)[..., ::2]],                    # LSE not contiguous
+        [torch.empty_like(q)],                                                     # missing LSE
+    ]
+    for outs in bad_sets:
+        with pytest.raises(ValueError):
+            binding._check_outs(outs, good, q)
