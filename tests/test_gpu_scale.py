@@ -5,7 +5,8 @@ the exp2 argument of the scores, into the score tangents and into gQ, gK.  Check
 against the fp64 oracle with the same scale, element by element, for the JVP, the forward,
 the zero-clean JVP and the backward, at a small scale (flat softmax), a moderate one and
 s = 1 with D = 128 (score standard deviation ~11: nearly one-hot rows, frequent moves of the
-reference max).  Tolerance: relative L2 1e-2 for bf16, 1e-4 for fp32.
+reference max).  Tolerance: relative L2 1e-2 for bf16, 1e-4 for fp32.  Also peaked rows
+from Q and K drawn with standard deviation 2-3.
 """
 import sys
 
@@ -97,3 +98,38 @@ def test_backward_with_scale(dt, s):
     _say(f"[scale] backward {dt} s={s} rel-L2 gQ={errs[0]:.2e} gK={errs[1]:.2e} gV={errs[2]:.2e} "
          f"Delta={errs[3]:.2e}")
     assert max(errs) <= TOL[dt], errs
+
+
+# Peaked rows (the stress variant of Q and K drawn with standard deviation 2-3, and a softmax
+# scale of 1): the tangent dO = (T - r O) / l subtracts nearly equal terms there, which
+# magnifies the bf16 rounding of H~; the errors stay inside the bf16 bar.
+
+
+def _peaked_inputs(w, seed, qk_std):
+    x = make_inputs(w, "cpu", seed)
+    for k in ("Q", "K"):
+        x[k] = (x[k].float() * qk_std).to(x[k].dtype)
+    return x
+
+
+@pytest.mark.parametrize("qk_std,s", [(1.0, 1.0), (2.5, None), (3.0, None), (2.0, 0.3)])
+def test_peaked_rows_tangent_error(qk_std, s):
+    w = _workload("bf16")
+    offs = list(w.offsets)
+    half = w.L // 2
+    _say(f"[peaked] Q, K std {qk_std}, scale {s or '1/sqrt(D)'}")
+    x = _peaked_inputs(w, 44, qk_std)
+    g = {k: v.cuda() for k, v in x.items()}
+    o, do, lse = attn_jvp_fwd(g["Q"], g["K"], g["V"], g["dQ"], g["dK"], g["dV"], w.kind, offs, scale=s)
+    tn = [g[k][:, :, half:].contiguous() for k in ("dQ", "dK", "dV")]
+    oz, don, lsez = attn_jvp_fwd_zero_clean(g["Q"], g["K"], g["V"], *tn, offs, scale=s)
+    torch.cuda.synchronize()
+    xs = [_np(x[k]) for k in ("Q", "K", "V", "dQ", "dK", "dV")]
+    O, dO, LSE = attention_jvp(*xs, w.kind, offs, scale=s)
+    xz = xs[:3] + [t[:, :, half:] for t in xs[3:]]
+    Oz, dOz, LSEz = attention_jvp_zero_clean(*xz, offs, scale=s)
+    errs = (_rel(_np(o), O), _rel(_np(do), dO), _rel(_np(lse), LSE), _rel(_np(don), dOz[:, :, half:]),
+            _rel(_np(oz), Oz))
+    _say(f"[peaked] std {qk_std} s={s} rel-L2 O={errs[0]:.2e} dO={errs[1]:.2e} LSE={errs[2]:.2e} "
+         f"zero-clean dOn={errs[3]:.2e} O={errs[4]:.2e}")
+    assert max(errs) <= TOL["bf16"], errs
