@@ -29,10 +29,11 @@
  *   keeps no per-call state, so calls are reentrant and may be captured in a
  *   HIP graph.  Inputs are never written.  Outputs must not overlap inputs or
  *   each other (checked by address range; overlap is ATTN_ERR_INVALID).
- * - Sizes: B, H, L >= 1, B * H <= 2^20; bf16 inputs need L * D <= 2^31 (the kernels
- *   address a head with 32-bit byte offsets) and ceil(L / 128) * B * H <= 2^31 - 1
- *   (work-groups of one launch); fp32 inputs need B * H <= 65535 (one grid row per
- *   (batch, head)).  Larger sizes are ATTN_ERR_INVALID.
+ * - Sizes: B, H, L >= 1, B * H <= 2^20, ceil(L / 128) * B * H <= 2^31 - 1 (work-groups
+ *   of one launch); the kernels address a head with 32-bit byte offsets, so bf16 inputs
+ *   need L * D <= 2^31 and fp32 inputs L * D <= 2^30; the fp32 backward also needs
+ *   B * H <= 65535 (it takes one grid row per (batch, head)).  Larger sizes are
+ *   ATTN_ERR_INVALID.
  * - Return codes: ATTN_OK, or ATTN_ERR_INVALID (bad pointer, size or layout),
  *   ATTN_ERR_UNSUPPORTED (dtype / head_dim not built), ATTN_ERR_HIP (a HIP
  *   launch error).  All argument and layout validation happens before any HIP
@@ -52,7 +53,7 @@ extern "C" {
 
 /* element types of Q, K, V, dQ, dK, dV, O, dO */
 enum {
-  ATTN_DTYPE_F32 = 0,  /* fp32 in, fp32 math (exact-path kernel), fp32 out; D in {64, 128} */
+  ATTN_DTYPE_F32 = 0,  /* fp32 in, fp32 math (fp32 matrix cores), fp32 out; D in {64, 128} */
   ATTN_DTYPE_BF16 = 1  /* bf16 in, bf16 MFMA with fp32 accumulation, bf16 out; D in {64, 128} */
 };
 

@@ -56,7 +56,9 @@ constexpr int kMfmaBr = 256;
 constexpr int kMfmaBrFwd = 128;
 constexpr int kMfmaBc = 32;
 
-// fp32 exact-path kernels: one wave per query row.
+// fp32 kernels: the forward and JVP take query tiles of kF32Br rows (4 waves x 32) on the
+// fp32 matrix cores; the backward's fp32 passes take one wave per query row or key.
+constexpr int kF32Br = 128;
 constexpr int kSimtRowsPerBlock = 4;
 
 // What a launch computes: the primal only, the JVP with tangents on every row (t0 = 0),

@@ -16,7 +16,7 @@ namespace {
 int launch(attn::Pass pass, int dtype, int D, const attn::AttnArgs& args, void* stream) {
   const hipError_t e = dtype == ATTN_DTYPE_BF16
                            ? attn::launch_mfma_bf16(args, D, pass, (hipStream_t)stream)
-                           : attn::launch_simt_f32(args, D, pass, (hipStream_t)stream);
+                           : attn::launch_mfma_f32(args, D, pass, (hipStream_t)stream);
   if (e != hipSuccess) return attn::set_error(ATTN_ERR_HIP, std::string("HIP launch failed: ") + hipGetErrorString(e));
   return ATTN_OK;
 }

@@ -8,7 +8,7 @@
 namespace attn {
 
 hipError_t launch_mfma_bf16(const AttnArgs& a, int D, Pass pass, hipStream_t stream);
-hipError_t launch_simt_f32(const AttnArgs& a, int D, Pass pass, hipStream_t stream);
+hipError_t launch_mfma_f32(const AttnArgs& a, int D, Pass pass, hipStream_t stream);
 
 // The backward is two launches on one stream: the query-tile pass (gQ and Delta, with
 // `qa` holding the query-tile order) and then the key-tile pass (gK and gV, with `ka`

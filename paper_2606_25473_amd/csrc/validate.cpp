@@ -22,22 +22,22 @@ struct Span {
 
 bool overlap(const Span& x, const Span& y) { return x.lo < y.hi && y.lo < x.hi; }
 
-// Size limits of the kernels (after the positivity checks): the bf16 kernels address a
-// head with 32-bit byte offsets and launch one work-group per tile of at least 128 rows
-// or keys and (batch, head) along x; the fp32 kernels launch one grid row per (batch,
-// head) along y.
-int check_sizes(int dtype, int B, int H, int L, int D) {
+// Size limits of the kernels (after the positivity checks): the kernels address a head with
+// 32-bit byte offsets and launch one work-group per tile of at least 128 rows or keys and
+// (batch, head) along x; the fp32 backward launches one grid row per (batch, head) along y.
+int check_sizes(int dtype, int B, int H, int L, int D, bool bwd) {
   const int64_t bh = (int64_t)B * H;
   if (bh > (int64_t)1 << 20) return fail(ATTN_ERR_INVALID, "B * H too large");
-  if (dtype == ATTN_DTYPE_BF16) {
-    if ((int64_t)L * D > (int64_t)1 << 31)
-      return fail(ATTN_ERR_INVALID, "bf16 needs L * D <= 2^31 (32-bit offsets within a head), got L = " +
-                                        std::to_string(L) + ", D = " + std::to_string(D));
-    if (((int64_t)L + 127) / 128 * bh > INT32_MAX)
-      return fail(ATTN_ERR_INVALID, "too many work-groups for one launch: ceil(L / 128) * B * H > 2^31 - 1");
-  } else if (bh > 65535) {
-    return fail(ATTN_ERR_INVALID, "fp32 needs B * H <= 65535, got " + std::to_string(bh));
-  }
+  // the kernels address a head with 32-bit byte offsets: 4 GiB per tensor and head
+  const int64_t max_ld = dtype == ATTN_DTYPE_BF16 ? (int64_t)1 << 31 : (int64_t)1 << 30;
+  if ((int64_t)L * D > max_ld)
+    return fail(ATTN_ERR_INVALID, std::string(dtype == ATTN_DTYPE_BF16 ? "bf16 needs L * D <= 2^31" : "fp32 needs L * D <= 2^30") +
+                                      " (32-bit offsets within a head), got L = " + std::to_string(L) +
+                                      ", D = " + std::to_string(D));
+  if (((int64_t)L + 127) / 128 * bh > INT32_MAX)
+    return fail(ATTN_ERR_INVALID, "too many work-groups for one launch: ceil(L / 128) * B * H > 2^31 - 1");
+  if (bwd && dtype == ATTN_DTYPE_F32 && bh > 65535)
+    return fail(ATTN_ERR_INVALID, "the fp32 backward needs B * H <= 65535, got " + std::to_string(bh));
   return ATTN_OK;
 }
 
@@ -61,7 +61,7 @@ int prepare(Pass pass, int dtype, int B, int H, int L, int D, const void* Q, con
   if (B <= 0 || H <= 0 || L <= 0)
     return fail(ATTN_ERR_INVALID, "B, H and L must be positive (B=" + std::to_string(B) +
                                       ", H=" + std::to_string(H) + ", L=" + std::to_string(L) + ")");
-  if (const int rc = check_sizes(dtype, B, H, L, D)) return rc;
+  if (const int rc = check_sizes(dtype, B, H, L, D, false)) return rc;
   if (!Q || !K || !V || !O || !LSE) return fail(ATTN_ERR_INVALID, "NULL tensor pointer");
   if (jvp && (!dQ || !dK || !dV || !dO)) return fail(ATTN_ERR_INVALID, "NULL tangent pointer");
   if (!layout) return fail(ATTN_ERR_INVALID, "layout is NULL");
@@ -104,10 +104,15 @@ int prepare(Pass pass, int dtype, int B, int H, int L, int D, const void* Q, con
   args->B = B; args->H = H; args->L = L;
   args->t0 = t0;
   args->scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt((float)D);
-  // the forward-only bf16 kernel takes 128-row tiles, the JVP kernels 256-row tiles
-  const int br = (pass == Pass::kFwd && dtype == ATTN_DTYPE_BF16) ? kMfmaBrFwd : kMfmaBr;
-  args->order = zc ? make_tile_order_zero_clean(args->gt, L, kMfmaBr, kMfmaBc, t0)
-                   : make_tile_order(layout, L, br);
+  // the bf16 forward-only kernel takes 128-row tiles, the bf16 JVP kernels 256-row tiles, the
+  // fp32 kernels 128-row tiles
+  if (dtype == ATTN_DTYPE_F32) {
+    args->order = make_tile_order(layout, L, kF32Br);
+  } else {
+    const int br = pass == Pass::kFwd ? kMfmaBrFwd : kMfmaBr;
+    args->order = zc ? make_tile_order_zero_clean(args->gt, L, kMfmaBr, kMfmaBc, t0)
+                     : make_tile_order(layout, L, br);
+  }
   return ATTN_OK;
 }
 
@@ -122,7 +127,7 @@ int prepare_bwd(int dtype, int B, int H, int L, int D, const void* Q, const void
   if (B <= 0 || H <= 0 || L <= 0)
     return fail(ATTN_ERR_INVALID, "B, H and L must be positive (B=" + std::to_string(B) +
                                       ", H=" + std::to_string(H) + ", L=" + std::to_string(L) + ")");
-  if (const int rc = check_sizes(dtype, B, H, L, D)) return rc;
+  if (const int rc = check_sizes(dtype, B, H, L, D, true)) return rc;
   const void* ins[6] = {Q, K, V, O, gO, LSE};
   const char* in_names[6] = {"Q", "K", "V", "O", "gO", "LSE"};
   void* outs[4] = {gQ, gK, gV, Delta};

@@ -2,7 +2,7 @@
 
 bf16: B * H = 2^20 (batch 1024 x 1024 heads of 32 tokens, D = 64): about a million
 work-groups per launch, mapped through the head-group / position order.  fp32: B * H = 65535,
-the most grid rows the fp32 kernels launch.  The JVP, the forward and the backward are checked
+the most grid rows the fp32 backward launches.  The JVP, the forward and the backward are checked
 on sampled (batch, head) pairs -- the first, the last, and seeded random ones -- against the
 oracle, element by element; every output must be finite.
 """

@@ -305,7 +305,8 @@ def _call(lib, **kw):
     (dict(L=(1 << 25) + 2, D=64, layout=make_layout("teacher_forcing", [0, (1 << 24) + 1])), 1, "2^31"),
     (dict(B=1024, H=1024, L=1 << 18, D=64), 1, "work-groups"),
     (dict(B=2, H=1 << 20), 1, "B * H too large"),
-    (dict(dtype=0, B=256, H=256, L=16), 1, "65535"),
+    (dict(dtype=0, L=(1 << 23) + 2, D=128, layout=make_layout("teacher_forcing", [0, (1 << 22) + 1])), 1,
+     "2^30"),
 ])
 @_no_gpu
 def test_invalid_arguments_are_rejected_before_any_hip_call(lib, kw, code, needle):
@@ -359,14 +360,22 @@ def test_backward_entry_point_validates(lib):
 
 @_no_gpu
 def test_largest_accepted_sizes_pass_the_size_checks(lib):
-    # the largest bf16 head (L * D = 2^31) and an fp32 launch of 65535 (batch, head) pairs pass
-    # the size checks: the first failure is then a deliberately bad layout (checked later)
+    # the largest bf16 head (L * D = 2^31), the largest fp32 head (L * D = 2^30) and an fp32
+    # forward of 2^20 (batch, head) pairs pass the size checks: the first failure is then a
+    # deliberately bad layout (checked later)
     bad = make_layout("teacher_forcing", [0, 16, 40])
     assert _call(lib, L=1 << 24, D=128, layout=bad) == 1 and "L = 2" in binding.last_error()
-    assert _call(lib, dtype=0, B=65535, H=1, L=16, layout=bad) == 1 and "L = 2" in binding.last_error()
+    assert _call(lib, dtype=0, L=1 << 23, D=128, layout=bad) == 1 and "L = 2" in binding.last_error()
+    assert _call(lib, dtype=0, B=1024, H=1024, L=16, layout=bad) == 1 and "L = 2" in binding.last_error()
     p = _ptrs(10, 2, 1, 1, 1 << 24, 128)
     rc = lib.attn_bwd(1, 1, 1, (1 << 24) + 2, 128, *p[:6], ctypes.byref(make_layout("full")), 0.0, *p[6:], None)
     assert rc == 1 and "2^31" in binding.last_error()
+    # the fp32 backward launches one grid row per (batch, head): at most 65535 of them
+    p = _ptrs(10, 4, 256, 256, 16, 64)
+    rc = lib.attn_bwd(0, 256, 256, 16, 64, *p[:6], ctypes.byref(bad), 0.0, *p[6:], None)
+    assert rc == 1 and "65535" in binding.last_error()
+    rc = lib.attn_bwd(0, 65535, 1, 16, 64, *p[:6], ctypes.byref(bad), 0.0, *p[6:], None)
+    assert rc == 1 and "L = 2" in binding.last_error()
 
 
 @_no_gpu
