@@ -31,8 +31,7 @@
  *   each other (checked by address range; overlap is ATTN_ERR_INVALID).
  * - Sizes: B, H, L >= 1, B * H <= 2^20, ceil(L / 128) * B * H <= 2^31 - 1 (work-groups
  *   of one launch); the kernels address a head with 32-bit byte offsets, so bf16 inputs
- *   need L * D <= 2^31 and fp32 inputs L * D <= 2^30; the fp32 backward also needs
- *   B * H <= 65535 (it takes one grid row per (batch, head)).  Larger sizes are
+ *   need L * D <= 2^31 and fp32 inputs L * D <= 2^30.  Larger sizes are
  *   ATTN_ERR_INVALID.
  * - Return codes: ATTN_OK, or ATTN_ERR_INVALID (bad pointer, size or layout),
  *   ATTN_ERR_UNSUPPORTED (dtype / head_dim not built), ATTN_ERR_HIP (a HIP

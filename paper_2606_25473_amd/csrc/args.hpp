@@ -56,10 +56,10 @@ constexpr int kMfmaBr = 256;
 constexpr int kMfmaBrFwd = 128;
 constexpr int kMfmaBc = 32;
 
-// fp32 kernels: the forward and JVP take query tiles of kF32Br rows (4 waves x 32) on the
-// fp32 matrix cores; the backward's fp32 passes take one wave per query row or key.
+// fp32 kernels (fp32 matrix cores): query tiles of kF32Br rows (8 waves x 16) for the
+// forward, the JVP and the backward's query-tile pass; the key-tile pass takes the same
+// kBwdKeysPerTile keys as the bf16 one (8 waves x 16).
 constexpr int kF32Br = 128;
-constexpr int kSimtRowsPerBlock = 4;
 
 // What a launch computes: the primal only, the JVP with tangents on every row (t0 = 0),
 // or the JVP whose tangents are zero on rows [0, t0) and stored for rows [t0, L) only.

@@ -20,8 +20,7 @@
 // (the scores S and gP are computed in both), against 10 D for a single pass that would
 // need atomic gQ updates.
 //
-// fp32 exact-path kernels (one wave per query row, then one wave per key) implement the
-// same two passes for the fp32 entry point.
+// The fp32 entry point runs the same two passes on fp32 matrix cores (attn_f32.hip).
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -270,21 +269,6 @@ void attn_bwd_dq_kernel(const BwdArgs a) {
 constexpr int KT = kBwdKeysPerTile;   // 128 keys per work-group (4 key groups of 32)
 
 constexpr int QB = kBwdRowsPerBlock;  // 64 query rows per block (2 halves of 32)
-
-// Direct global -> LDS load of 4 bytes per lane (lane l's bytes land at lds + 4 l);
-// same contract as lds_load16.
-__device__ __forceinline__ void lds_load4(const void* gbase, unsigned byte_off, unsigned lds) {
-  unsigned saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %3\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dword %1, %2\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(byte_off), "s"(gbase), "s"(__builtin_amdgcn_readfirstlane(lds))
-      : "memory");
-}
 
 template <int D>
 struct KGeo {
@@ -539,122 +523,6 @@ void attn_bwd_dkdv_kernel(const BwdArgs a) {
   }
 }
 
-// ---------------------------------------------------------------- fp32 exact path
-
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
-  return x;
-}
-
-// One wave per query row: Delta and gQ over the row's key ranges, key by key.
-template <int D>
-__global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_bwd_simt_dq_kernel(const BwdArgs a) {
-  constexpr int E = D / 64;
-  const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * kSimtRowsPerBlock + (threadIdx.x >> 6);
-  const int bh = blockIdx.y;
-  const int L = a.L;
-  if (row >= L) return;
-  const size_t head = (size_t)bh * L * D;
-  const float* Q = (const float*)a.Q + head;
-  const float* K = (const float*)a.K + head;
-  const float* V = (const float*)a.V + head;
-  const float* O = (const float*)a.O + head;
-  const float* gO = (const float*)a.gO + head;
-  const int g = find_group(a.gt, row);
-  const int r_first = a.gt.r_begin[g], r_last = a.gt.r_begin[g + 1];  // the group's key ranges
-  float q[E], go[E], acc[E];
-  float dp = 0.f;
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const size_t i = (size_t)row * D + lane + 64 * e;
-    q[e] = Q[i];
-    go[e] = gO[i];
-    acc[e] = 0.f;
-    dp += go[e] * O[i];
-  }
-  const float delta = wave_sum(dp);
-  const float lse = a.LSE[(size_t)bh * L + row];
-  const float sc = a.scale;
-  for (int ri = r_first; ri < r_last; ++ri) {
-    for (int k = a.gt.k[2 * ri]; k < a.gt.k[2 * ri + 1]; ++k) {
-      float s = 0.f, gp = 0.f;
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        s += q[e] * K[(size_t)k * D + lane + 64 * e];
-        gp += go[e] * V[(size_t)k * D + lane + 64 * e];
-      }
-      s = wave_sum(s) * sc;
-      gp = wave_sum(gp);
-      const float gs = expf(s - lse) * (gp - delta);
-#pragma unroll
-      for (int e = 0; e < E; ++e) acc[e] += gs * K[(size_t)k * D + lane + 64 * e];
-    }
-  }
-  float* gQ = (float*)a.gQ + head + (size_t)row * D;
-#pragma unroll
-  for (int e = 0; e < E; ++e) gQ[lane + 64 * e] = sc * acc[e];
-  if (lane == 0) a.Delta[(size_t)bh * L + row] = delta;
-}
-
-// One wave per key: gK and gV over the queries of the groups that admit the key.
-template <int D>
-__global__ __launch_bounds__(64 * kSimtRowsPerBlock) void attn_bwd_simt_dkdv_kernel(const BwdArgs a) {
-  constexpr int E = D / 64;
-  const int lane = threadIdx.x & 63;
-  const int key = blockIdx.x * kSimtRowsPerBlock + (threadIdx.x >> 6);
-  const int bh = blockIdx.y;
-  const int L = a.L;
-  if (key >= L) return;
-  const size_t head = (size_t)bh * L * D;
-  const float* Q = (const float*)a.Q + head;
-  const float* K = (const float*)a.K + head;
-  const float* V = (const float*)a.V + head;
-  const float* gO = (const float*)a.gO + head;
-  const float* LSE = a.LSE + (size_t)bh * L;
-  const float* Dl = a.Delta + (size_t)bh * L;
-  float k[E], v[E], gk[E], gv[E];
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    k[e] = K[(size_t)key * D + lane + 64 * e];
-    v[e] = V[(size_t)key * D + lane + 64 * e];
-    gk[e] = 0.f;
-    gv[e] = 0.f;
-  }
-  const float sc = a.scale;
-  // the queries of every group that admits this key
-  for (int g = 0; g < a.gt.n; ++g) {
-    bool hit = false;
-    for (int ri = a.gt.r_begin[g]; ri < a.gt.r_begin[g + 1]; ++ri) hit |= key >= a.gt.k[2 * ri] && key < a.gt.k[2 * ri + 1];
-    if (!hit) continue;
-    for (int q = group_q_begin(a.gt, g); q < a.gt.q_end[g]; ++q) {
-      float s = 0.f, gp = 0.f;
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        s += Q[(size_t)q * D + lane + 64 * e] * k[e];
-        gp += gO[(size_t)q * D + lane + 64 * e] * v[e];
-      }
-      s = wave_sum(s) * sc;
-      gp = wave_sum(gp);
-      const float p = expf(s - LSE[q]);
-      const float gs = p * (gp - Dl[q]);
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        gk[e] += gs * Q[(size_t)q * D + lane + 64 * e];
-        gv[e] += p * gO[(size_t)q * D + lane + 64 * e];
-      }
-    }
-  }
-  float* gK = (float*)a.gK + head + (size_t)key * D;
-  float* gV = (float*)a.gV + head + (size_t)key * D;
-#pragma unroll
-  for (int e = 0; e < E; ++e) {
-    gK[lane + 64 * e] = sc * gk[e];
-    gV[lane + 64 * e] = gv[e];
-  }
-}
-
 }  // namespace
 
 hipError_t launch_bwd_mfma_bf16(const BwdArgs& qa, const BwdArgs& ka, int D, hipStream_t stream) {
@@ -666,19 +534,6 @@ hipError_t launch_bwd_mfma_bf16(const BwdArgs& qa, const BwdArgs& ka, int D, hip
   } else {
     hipLaunchKernelGGL((attn_bwd_dq_kernel<64>), gq, block, 0, stream, qa);
     hipLaunchKernelGGL((attn_bwd_dkdv_kernel<64>), gk, block, 0, stream, ka);
-  }
-  return hipGetLastError();
-}
-
-hipError_t launch_bwd_simt_f32(const BwdArgs& qa, const BwdArgs& ka, int D, hipStream_t stream) {
-  const dim3 grid((unsigned)((qa.L + kSimtRowsPerBlock - 1) / kSimtRowsPerBlock), (unsigned)(qa.B * qa.H));
-  const dim3 block(64 * kSimtRowsPerBlock);
-  if (D == 128) {
-    hipLaunchKernelGGL((attn_bwd_simt_dq_kernel<128>), grid, block, 0, stream, qa);
-    hipLaunchKernelGGL((attn_bwd_simt_dkdv_kernel<128>), grid, block, 0, stream, ka);
-  } else {
-    hipLaunchKernelGGL((attn_bwd_simt_dq_kernel<64>), grid, block, 0, stream, qa);
-    hipLaunchKernelGGL((attn_bwd_simt_dkdv_kernel<64>), grid, block, 0, stream, ka);
   }
   return hipGetLastError();
 }

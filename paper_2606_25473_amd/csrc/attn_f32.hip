@@ -76,6 +76,30 @@ __device__ __forceinline__ f32x4 mfma16(float a, float b, f32x4 c) {
 // value of lane l ^ 16 and l ^ 32 (row statistics: a query's keys lie in four lanes)
 __device__ __forceinline__ float xor16(float x) { return __shfl_xor(x, 16, 64); }
 
+// Rows [row0, row0 + 32) of a [rows, D] fp32 tensor (rows clamped to [0, rmax]: finite
+// data that the kernels mask or never store) into the swizzled LDS tile at dst, by 1 KiB
+// direct loads.  Lane l of a load lands at byte 16 l, i.e. physical row 16 l / ROWB and
+// physical chunk p, and fetches the logical chunk p ^ swizzle(row).  Load j is issued by
+// wave j % NW.
+template <int D>
+__device__ __forceinline__ void dma_tile(const float* src, int row0, int rmax, unsigned dst, int wave,
+                                         int lane) {
+  using G = FGeo<D>;
+  constexpr int RPI = 1024 / G::ROWB;
+  const int r = (lane * 16) / G::ROWB;
+  const int p = ((lane * 16) % G::ROWB) >> 4;
+#pragma unroll
+  for (int j0 = 0; j0 < G::IPT; j0 += NW) {
+    const int j = j0 + wave;
+    if (G::IPT % NW == 0 || j < G::IPT) {
+      const int rr = j * RPI + r;
+      const unsigned grow = (unsigned)imin(imax(row0 + rr, 0), rmax);
+      const unsigned off = (grow * D + (unsigned)((p ^ fswz(rr)) * 4)) * 4u;
+      lds_load16(src, off, dst + (unsigned)(j * 1024));
+    }
+  }
+}
+
 template <int D, bool JVP>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_f32_kernel(const AttnArgs a) {
@@ -137,32 +161,14 @@ void attn_f32_kernel(const AttnArgs a) {
     }
   }
 
-  // global -> LDS: one 1 KiB direct load per wave instruction; lane l lands at byte 16 l,
-  // i.e. physical row 16 l / ROWB, physical chunk p, and fetches the logical chunk
-  // p ^ swizzle(row).  Rows past the end are clamped (finite data; masked or unstored).
-  constexpr int RPI = 1024 / G::ROWB;
-  const int dma_r = (lane * 16) / G::ROWB;
-  const int dma_p = ((lane * 16) % G::ROWB) >> 4;
-  auto dma_tile = [&](const float* src, int row0, int rmax, unsigned dst) {
-#pragma unroll
-    for (int j0 = 0; j0 < G::IPT; j0 += NW) {
-      const int j = j0 + wave;
-      if (G::IPT % NW == 0 || j < G::IPT) {
-        const int rr = j * RPI + dma_r;
-        const unsigned grow = (unsigned)imin(imax(row0 + rr, 0), rmax);
-        const unsigned off = (grow * D + (unsigned)((dma_p ^ fswz(rr)) * 4)) * 4u;
-        lds_load16(src, off, dst + (unsigned)(j * 1024));
-      }
-    }
-  };
   const unsigned st_lds = __builtin_amdgcn_readfirstlane(lds_addr(stages));
   auto dma_block = [&](int kb, unsigned st) {
     const int k0 = kb * BC;
-    dma_tile(Kg, k0, L - 1, st);
-    dma_tile(Vg, k0, L - 1, st + TB);
+    dma_tile<D>(Kg, k0, L - 1, st, wave, lane);
+    dma_tile<D>(Vg, k0, L - 1, st + TB, wave, lane);
     if constexpr (JVP) {
-      dma_tile(dKg, k0 - t0, Lt - 1, st + 2 * TB);
-      dma_tile(dVg, k0 - t0, Lt - 1, st + 3 * TB);
+      dma_tile<D>(dKg, k0 - t0, Lt - 1, st + 2 * TB, wave, lane);
+      dma_tile<D>(dVg, k0 - t0, Lt - 1, st + 3 * TB, wave, lane);
     }
   };
 
@@ -351,6 +357,359 @@ void attn_f32_kernel(const AttnArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- backward
+//
+// Reverse mode for a cotangent gO of O, P recomputed from the saved LSE:
+//   Delta = rowsum(gO o O), gP = gO V^T, gS = P o (gP - Delta),
+//   gQ = s gS K, gK = s gS^T Q, gV = P^T gO,
+// in two deterministic passes with the geometry of the forward (no atomics).
+
+// Query-tile pass: a work-group owns 128 query rows (16 per wave), computes Delta for
+// them, and streams the key blocks of its plan (K, V tiles): S^T = K Q^T and
+// gP^T = V gO^T with the lane's quarter rows of Q and gO as B operands, then
+// gQ^T += K^T gS^T with gS^T as B operand as it stands (the output pattern of the forward).
+// 6 D flop per pair of matrix work.
+template <int D>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_f32_bwd_dq_kernel(const BwdArgs a) {
+  using G = FGeo<D>;
+  constexpr int TB = G::TILEB;
+  constexpr int SB = 2 * TB;  // stage: K, V tiles
+  __shared__ __attribute__((aligned(1024))) char stages[2 * SB];
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const int g = lane >> 4;
+  const int c16 = lane & 15;
+  const int L = a.L;
+
+  const TileSlot sl = slot_of(blockIdx.x, a.B * a.H, a.order.nt, kHeadGroup);
+  const int bh = sl.bh;
+  const int qtile = tile_of(a.order, sl.pos);
+  const size_t head = (size_t)bh * L * D;
+  const float* __restrict__ Qg = (const float*)a.Q + head;
+  const float* __restrict__ Kg = (const float*)a.K + head;
+  const float* __restrict__ Vg = (const float*)a.V + head;
+  const float* __restrict__ Og = (const float*)a.O + head;
+  const float* __restrict__ gOg = (const float*)a.gO + head;
+
+  const int q0 = qtile * BR;
+  const int q1 = q0 + BR < L ? q0 + BR : L;
+  const TilePlan plan = plan_tile(a.gt, q0, q1, BC);
+  const int nblk = plan_num_blocks(plan);
+
+  const int row = q0 + wave * QW + c16;
+  const int rowc = imin(row, L - 1);
+  const int wrow0 = imin(q0 + wave * QW, L - 1);
+  const int wg0 = find_group(a.gt, wrow0), wg1 = find_group(a.gt, imin(wrow0 + QW - 1, L - 1));
+
+  // quarter rows d = g D/4 + s of Q and gO; Delta from the same quarters of gO and O
+  float qv[G::QS], gov[G::QS];
+  float dpart = 0.f;
+  {
+    const size_t o = (size_t)rowc * D + g * G::QS;
+#pragma unroll
+    for (int s = 0; s < G::QS; s += 4) {
+      const f32x4 vq = *(const f32x4*)(Qg + o + s);
+      const f32x4 vg = *(const f32x4*)(gOg + o + s);
+      const f32x4 vo = *(const f32x4*)(Og + o + s);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        qv[s + e] = vq[e];
+        gov[s + e] = vg[e];
+        dpart = fmaf(vg[e], vo[e], dpart);
+      }
+    }
+  }
+  float delta = dpart + xor16(dpart);
+  delta += xor32(delta);
+  // LSE in log2 units.  A row without admissible keys has LSE = -inf: exp2 then gives
+  // +inf, which the mask replaces by 0 (such a row makes no block of its tile full).
+  const float lse2 = a.LSE[(size_t)bh * L + rowc] * kLog2e;
+  const float c2 = a.scale * kLog2e;
+
+  const unsigned st_lds = __builtin_amdgcn_readfirstlane(lds_addr(stages));
+  auto dma_block = [&](int kb, unsigned st) {
+    dma_tile<D>(Kg, kb * BC, L - 1, st, wave, lane);
+    dma_tile<D>(Vg, kb * BC, L - 1, st + TB, wave, lane);
+  };
+
+  f32x4 gq[G::DT];
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt) gq[dt] = f32x4{};
+
+  if (nblk > 0) dma_block(plan_block(plan, 0), st_lds);
+  __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): also the operand loads above
+  __syncthreads();
+
+  for (int it = 0; it < nblk; ++it) {
+    const unsigned cur = st_lds + (unsigned)((it & 1) * SB);
+    if (it + 1 < nblk) dma_block(plan_block(plan, it + 1), st_lds + (unsigned)(((it + 1) & 1) * SB));
+    const int k0 = plan_block(plan, it) * BC;
+
+    // S^T = K Q^T and gP^T = V gO^T per 16-key half; operands read one group ahead
+    f32x4 S[2] = {f32x4{}, f32x4{}}, GP[2] = {f32x4{}, f32x4{}};
+    {
+      constexpr int NU = G::QS / 4;
+      f32x4 kc[2][2], vc[2][2];
+      auto read = [&](int u) {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+          const unsigned o = foff<D>(16 * kt + c16, g * (G::NCH / 4) + u);
+          kc[u & 1][kt] = *(lds_f32x4*)(uintptr_t)(cur + o);
+          vc[u & 1][kt] = *(lds_f32x4*)(uintptr_t)(cur + TB + o);
+        }
+      };
+      read(0);
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        if (u + 1 < NU) read(u + 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int kt = 0; kt < 2; ++kt) {
+            S[kt] = mfma16(kc[u & 1][kt][e], qv[4 * u + e], S[kt]);
+            GP[kt] = mfma16(vc[u & 1][kt][e], gov[4 * u + e], GP[kt]);
+          }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+
+    // P and gS; slot i = 4 kt + j holds key k0 + 16 kt + 4 g + j
+    float p[8], gs[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) p[i] = __builtin_amdgcn_exp2f(fmaf(S[i >> 2][i & 3], c2, -lse2));
+    if (!block_is_full(plan, k0, BC, L)) {
+      const uint32_t bits = row_bits(a.gt, wg0, wg1, row, k0) >> (4 * g);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) p[i] = ((bits >> (16 * (i >> 2) + (i & 3))) & 1u) ? p[i] : 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) gs[i] = p[i] * (GP[i >> 2][i & 3] - delta);
+
+    // gQ^T += K^T gS^T: step i contracts key 16 kt + 4 g + j of group g (the lane's slot i)
+    {
+      constexpr int NCR = G::DT / 4;
+      f32x4 kr[2][NCR];
+      auto read = [&](int i) {
+        const int key = 16 * (i >> 2) + 4 * g + (i & 3);
+#pragma unroll
+        for (int c = 0; c < NCR; ++c) kr[i & 1][c] = *(lds_f32x4*)(uintptr_t)(cur + foff<D>(key, c16 + 16 * c));
+      };
+      read(0);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        if (i + 1 < 8) read(i + 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int dt = 0; dt < G::DT; ++dt) gq[dt] = mfma16(kr[i & 1][dt >> 2][dt & 3], gs[i], gq[dt]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  }
+
+  // gQ = s gQ^T^T: tile dt slot j holds d = 4 m + dt%4 + 64 (dt/4), m = 4 g + j
+  if (row < L) {
+    float* gQg = (float*)a.gQ + head + (size_t)row * D;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int c = 0; c < G::DT / 4; ++c) {
+        f32x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = a.scale * gq[4 * c + e][j];
+        *(f32x4*)(gQg + 4 * (4 * g + j) + 64 * c) = v;
+      }
+    if (g == 0) a.Delta[(size_t)bh * L + row] = delta;
+  }
+}
+
+// Key-tile pass: a work-group owns 128 keys (16 per wave) and streams the 32-row query
+// blocks of the groups that admit some of them (the query-group table's key-tile plan):
+// Q, gO tiles and the blocks' LSE and Delta.  S = Q K^T and gP = gO V^T with the lane's
+// quarter rows of K and V as B operands put one key in each lane (16 queries per half),
+// so gV^T += gO^T P and gK^T += Q^T gS take P and gS as B operands as they stand.
+// 8 D flop per pair of matrix work.
+template <int D>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_f32_bwd_dkdv_kernel(const BwdArgs a) {
+  using G = FGeo<D>;
+  constexpr int TB = G::TILEB;
+  constexpr int SB = 2 * TB + 2 * 256;  // stage: Q, gO tiles, LSE and Delta (64 floats each)
+  static_assert(SB % 512 == 0, "stages start on whole LDS rows");
+  __shared__ __attribute__((aligned(1024))) char stages[2 * SB];
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const int g = lane >> 4;
+  const int c16 = lane & 15;
+  const int L = a.L;
+
+  const TileSlot sl = slot_of(blockIdx.x, a.B * a.H, a.order.nt, kHeadGroupWide);
+  const int bh = sl.bh;
+  const int ktile = tile_of(a.order, sl.pos);
+  const size_t head = (size_t)bh * L * D;
+  const float* __restrict__ Qg = (const float*)a.Q + head;
+  const float* __restrict__ Kg = (const float*)a.K + head;
+  const float* __restrict__ Vg = (const float*)a.V + head;
+  const float* __restrict__ gOg = (const float*)a.gO + head;
+  const float* __restrict__ LSEg = a.LSE + (size_t)bh * L;
+  const float* __restrict__ Dg = a.Delta + (size_t)bh * L;
+
+  const int k0 = ktile * BR;
+  const int k1 = k0 + BR < L ? k0 + BR : L;
+  const TilePlan plan = plan_key_tile(a.gt, k0, k1, BC);
+  const int nblk = plan_num_blocks(plan);
+
+  const int key = k0 + wave * QW + c16;
+  const int keyc = imin(key, L - 1);
+  float kv[G::QS], vv[G::QS];
+  {
+    const size_t o = (size_t)keyc * D + g * G::QS;
+#pragma unroll
+    for (int s = 0; s < G::QS; s += 4) {
+      const f32x4 vk = *(const f32x4*)(Kg + o + s);
+      const f32x4 vw = *(const f32x4*)(Vg + o + s);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        kv[s + e] = vk[e];
+        vv[s + e] = vw[e];
+      }
+    }
+  }
+  const float c2 = a.scale * kLog2e;
+
+  const unsigned st_lds = __builtin_amdgcn_readfirstlane(lds_addr(stages));
+  auto dma_block = [&](int qb, unsigned st) {
+    const int r0 = qb * BC;
+    dma_tile<D>(Qg, r0, L - 1, st, wave, lane);
+    dma_tile<D>(gOg, r0, L - 1, st + TB, wave, lane);
+    // 64 values each (rows past the block: clamped, never read)
+    const unsigned roff = (unsigned)imin(r0 + lane, L - 1) * 4u;
+    if (wave == NW - 2) lds_load4(LSEg, roff, st + 2 * TB);
+    if (wave == NW - 1) lds_load4(Dg, roff, st + 2 * TB + 256);
+  };
+
+  f32x4 gk[G::DT], gv[G::DT];
+#pragma unroll
+  for (int dt = 0; dt < G::DT; ++dt) {
+    gk[dt] = f32x4{};
+    gv[dt] = f32x4{};
+  }
+
+  if (nblk > 0) dma_block(plan_block(plan, 0), st_lds);
+  __builtin_amdgcn_s_waitcnt(0xF70);
+  __syncthreads();
+
+  for (int it = 0; it < nblk; ++it) {
+    const unsigned cur = st_lds + (unsigned)((it & 1) * SB);
+    if (it + 1 < nblk) dma_block(plan_block(plan, it + 1), st_lds + (unsigned)(((it + 1) & 1) * SB));
+    const int q0b = plan_block(plan, it) * BC;
+
+    // S = Q K^T and gP = gO V^T per 16-row half qt: the lane holds rows 16 qt + 4 g + j
+    // of its key
+    f32x4 S[2] = {f32x4{}, f32x4{}}, GP[2] = {f32x4{}, f32x4{}};
+    {
+      constexpr int NU = G::QS / 4;
+      f32x4 qc[2][2], gc[2][2];
+      auto read = [&](int u) {
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+          const unsigned o = foff<D>(16 * qt + c16, g * (G::NCH / 4) + u);
+          qc[u & 1][qt] = *(lds_f32x4*)(uintptr_t)(cur + o);
+          gc[u & 1][qt] = *(lds_f32x4*)(uintptr_t)(cur + TB + o);
+        }
+      };
+      read(0);
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        if (u + 1 < NU) read(u + 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int qt = 0; qt < 2; ++qt) {
+            S[qt] = mfma16(qc[u & 1][qt][e], kv[4 * u + e], S[qt]);
+            GP[qt] = mfma16(gc[u & 1][qt][e], vv[4 * u + e], GP[qt]);
+          }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+
+    // LSE and Delta of the lane's rows 16 qt + 4 g .. + 3; P and gS
+    float p[8], gs[8];
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      const f32x4 lv = *(lds_f32x4*)(uintptr_t)(cur + 2 * TB + 4 * (16 * qt + 4 * g));
+      const f32x4 dv = *(lds_f32x4*)(uintptr_t)(cur + 2 * TB + 256 + 4 * (16 * qt + 4 * g));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = 4 * qt + j;
+        p[i] = __builtin_amdgcn_exp2f(fmaf(S[qt][j], c2, -lv[j] * kLog2e));
+        gs[i] = dv[j];
+      }
+    }
+    if (!block_is_full(plan, q0b, BC, L)) {  // rows without admissible keys end up here too
+      const uint32_t bits = key_bits(a.gt, key, q0b, L) >> (4 * g);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) p[i] = ((bits >> (16 * (i >> 2) + (i & 3))) & 1u) ? p[i] : 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) gs[i] = p[i] * (GP[i >> 2][i & 3] - gs[i]);
+
+    // gV^T += gO^T P and gK^T += Q^T gS: step i contracts row 16 qt + 4 g + j of group g
+    {
+      constexpr int NCR = G::DT / 4;
+      f32x4 gr[2][NCR], qr[2][NCR];
+      auto read = [&](int i) {
+        const int r = 16 * (i >> 2) + 4 * g + (i & 3);
+#pragma unroll
+        for (int c = 0; c < NCR; ++c) {
+          const unsigned o = foff<D>(r, c16 + 16 * c);
+          qr[i & 1][c] = *(lds_f32x4*)(uintptr_t)(cur + o);
+          gr[i & 1][c] = *(lds_f32x4*)(uintptr_t)(cur + TB + o);
+        }
+      };
+      read(0);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        if (i + 1 < 8) read(i + 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int dt = 0; dt < G::DT; ++dt) {
+          gv[dt] = mfma16(gr[i & 1][dt >> 2][dt & 3], p[i], gv[dt]);
+          gk[dt] = mfma16(qr[i & 1][dt >> 2][dt & 3], gs[i], gk[dt]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  }
+
+  if (key < L) {
+    float* gKg = (float*)a.gK + head + (size_t)key * D;
+    float* gVg = (float*)a.gV + head + (size_t)key * D;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int c = 0; c < G::DT / 4; ++c) {
+        f32x4 vk, vw;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          vk[e] = a.scale * gk[4 * c + e][j];
+          vw[e] = gv[4 * c + e][j];
+        }
+        const int d = 4 * (4 * g + j) + 64 * c;
+        *(f32x4*)(gKg + d) = vk;
+        *(f32x4*)(gVg + d) = vw;
+      }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_mfma_f32(const AttnArgs& a, int D, Pass pass, hipStream_t stream) {
@@ -363,6 +722,19 @@ hipError_t launch_mfma_f32(const AttnArgs& a, int D, Pass pass, hipStream_t stre
   } else {
     if (jvp) hipLaunchKernelGGL((attn_f32_kernel<64, true>), grid, block, 0, stream, a);
     else hipLaunchKernelGGL((attn_f32_kernel<64, false>), grid, block, 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_mfma_f32(const BwdArgs& qa, const BwdArgs& ka, int D, hipStream_t stream) {
+  const dim3 gq((unsigned)(qa.order.nt * qa.B * qa.H)), gk((unsigned)(ka.order.nt * ka.B * ka.H));
+  const dim3 block(64 * NW);
+  if (D == 128) {
+    hipLaunchKernelGGL((attn_f32_bwd_dq_kernel<128>), gq, block, 0, stream, qa);
+    hipLaunchKernelGGL((attn_f32_bwd_dkdv_kernel<128>), gk, block, 0, stream, ka);
+  } else {
+    hipLaunchKernelGGL((attn_f32_bwd_dq_kernel<64>), gq, block, 0, stream, qa);
+    hipLaunchKernelGGL((attn_f32_bwd_dkdv_kernel<64>), gk, block, 0, stream, ka);
   }
   return hipGetLastError();
 }

@@ -63,7 +63,7 @@ int attn_bwd(int dtype, int B, int H, int L, int D, const void* Q, const void* K
                                    Delta, &qa, &ka);
   if (rc != ATTN_OK) return rc;
   const hipError_t e = dtype == ATTN_DTYPE_BF16 ? attn::launch_bwd_mfma_bf16(qa, ka, D, (hipStream_t)stream)
-                                                : attn::launch_bwd_simt_f32(qa, ka, D, (hipStream_t)stream);
+                                                : attn::launch_bwd_mfma_f32(qa, ka, D, (hipStream_t)stream);
   if (e != hipSuccess) return attn::set_error(ATTN_ERR_HIP, std::string("HIP launch failed: ") + hipGetErrorString(e));
   return ATTN_OK;
 }

@@ -14,6 +14,6 @@ hipError_t launch_mfma_f32(const AttnArgs& a, int D, Pass pass, hipStream_t stre
 // `qa` holding the query-tile order) and then the key-tile pass (gK and gV, with `ka`
 // holding the key-tile order), which reads Delta.
 hipError_t launch_bwd_mfma_bf16(const BwdArgs& qa, const BwdArgs& ka, int D, hipStream_t stream);
-hipError_t launch_bwd_simt_f32(const BwdArgs& qa, const BwdArgs& ka, int D, hipStream_t stream);
+hipError_t launch_bwd_mfma_f32(const BwdArgs& qa, const BwdArgs& ka, int D, hipStream_t stream);
 
 }  // namespace attn

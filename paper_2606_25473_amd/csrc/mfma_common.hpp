@@ -116,6 +116,21 @@ __device__ __forceinline__ void lds_load16(const void* gbase, unsigned byte_off,
       : "memory");
 }
 
+// Direct global -> LDS load of 4 bytes per lane (lane l's bytes land at lds + 4 l);
+// same contract as lds_load16.
+__device__ __forceinline__ void lds_load4(const void* gbase, unsigned byte_off, unsigned lds) {
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dword %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(byte_off), "s"(gbase), "s"(__builtin_amdgcn_readfirstlane(lds))
+      : "memory");
+}
+
 __device__ __forceinline__ unsigned lds_addr(const void* p) {
   return (unsigned)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }

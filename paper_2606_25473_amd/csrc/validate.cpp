@@ -24,8 +24,8 @@ bool overlap(const Span& x, const Span& y) { return x.lo < y.hi && y.lo < x.hi; 
 
 // Size limits of the kernels (after the positivity checks): the kernels address a head with
 // 32-bit byte offsets and launch one work-group per tile of at least 128 rows or keys and
-// (batch, head) along x; the fp32 backward launches one grid row per (batch, head) along y.
-int check_sizes(int dtype, int B, int H, int L, int D, bool bwd) {
+// (batch, head), in one grid dimension.
+int check_sizes(int dtype, int B, int H, int L, int D) {
   const int64_t bh = (int64_t)B * H;
   if (bh > (int64_t)1 << 20) return fail(ATTN_ERR_INVALID, "B * H too large");
   // the kernels address a head with 32-bit byte offsets: 4 GiB per tensor and head
@@ -36,8 +36,6 @@ int check_sizes(int dtype, int B, int H, int L, int D, bool bwd) {
                                       ", D = " + std::to_string(D));
   if (((int64_t)L + 127) / 128 * bh > INT32_MAX)
     return fail(ATTN_ERR_INVALID, "too many work-groups for one launch: ceil(L / 128) * B * H > 2^31 - 1");
-  if (bwd && dtype == ATTN_DTYPE_F32 && bh > 65535)
-    return fail(ATTN_ERR_INVALID, "the fp32 backward needs B * H <= 65535, got " + std::to_string(bh));
   return ATTN_OK;
 }
 
@@ -61,7 +59,7 @@ int prepare(Pass pass, int dtype, int B, int H, int L, int D, const void* Q, con
   if (B <= 0 || H <= 0 || L <= 0)
     return fail(ATTN_ERR_INVALID, "B, H and L must be positive (B=" + std::to_string(B) +
                                       ", H=" + std::to_string(H) + ", L=" + std::to_string(L) + ")");
-  if (const int rc = check_sizes(dtype, B, H, L, D, false)) return rc;
+  if (const int rc = check_sizes(dtype, B, H, L, D)) return rc;
   if (!Q || !K || !V || !O || !LSE) return fail(ATTN_ERR_INVALID, "NULL tensor pointer");
   if (jvp && (!dQ || !dK || !dV || !dO)) return fail(ATTN_ERR_INVALID, "NULL tangent pointer");
   if (!layout) return fail(ATTN_ERR_INVALID, "layout is NULL");
@@ -127,7 +125,7 @@ int prepare_bwd(int dtype, int B, int H, int L, int D, const void* Q, const void
   if (B <= 0 || H <= 0 || L <= 0)
     return fail(ATTN_ERR_INVALID, "B, H and L must be positive (B=" + std::to_string(B) +
                                       ", H=" + std::to_string(H) + ", L=" + std::to_string(L) + ")");
-  if (const int rc = check_sizes(dtype, B, H, L, D, true)) return rc;
+  if (const int rc = check_sizes(dtype, B, H, L, D)) return rc;
   const void* ins[6] = {Q, K, V, O, gO, LSE};
   const char* in_names[6] = {"Q", "K", "V", "O", "gO", "LSE"};
   void* outs[4] = {gQ, gK, gV, Delta};
@@ -166,7 +164,7 @@ int prepare_bwd(int dtype, int B, int H, int L, int D, const void* Q, const void
   qa->gQ = ka->gQ = gQ; qa->gK = ka->gK = gK; qa->gV = ka->gV = gV; qa->Delta = ka->Delta = Delta;
   qa->B = ka->B = B; qa->H = ka->H = H; qa->L = ka->L = L;
   qa->scale = ka->scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt((float)D);
-  qa->order = make_tile_order(layout, L, kMfmaBr);
+  qa->order = make_tile_order(layout, L, dtype == ATTN_DTYPE_F32 ? kF32Br : kMfmaBr);
   // key tiles: for the built-in layouts the work per key tile falls with the key index
   // (earlier keys are seen by more queries), so the natural order is heaviest first
   ka->order = TileOrder{};

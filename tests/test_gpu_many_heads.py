@@ -1,8 +1,7 @@
 """The largest head counts the boundary accepts (marked ``gpu``).
 
-bf16: B * H = 2^20 (batch 1024 x 1024 heads of 32 tokens, D = 64): about a million
-work-groups per launch, mapped through the head-group / position order.  fp32: B * H = 65535,
-the most grid rows the fp32 backward launches.  The JVP, the forward and the backward are checked
+B * H = 2^20 (batch 1024 x 1024 heads of 32 tokens, D = 64) in bf16 and in fp32: about a
+million work-groups per launch, mapped through the head-group / position order.  The JVP, the forward and the backward are checked
 on sampled (batch, head) pairs -- the first, the last, and seeded random ones -- against the
 oracle, element by element; every output must be finite.
 """
@@ -33,7 +32,7 @@ def _rel(x, ref):
     return float(np.linalg.norm(np.asarray(x) - np.asarray(ref)) / max(np.linalg.norm(ref), 1e-300))
 
 
-@pytest.mark.parametrize("dt,B,H,C", [("bf16", 1024, 1024, 8), ("f32", 65535, 1, 8)])
+@pytest.mark.parametrize("dt,B,H,C", [("bf16", 1024, 1024, 8), ("f32", 1024, 1024, 8)])
 def test_largest_head_count(dt, B, H, C):
     w = custom_workload(f"many_heads_{dt}", B, H, 64, dt, MASK_TEACHER_FORCING, 2, C, tangent_std=0.5)
     offs = list(w.offsets)
@@ -61,4 +60,6 @@ def test_largest_head_count(dt, B, H, C):
     _say(f"[many-heads] {dt} {len(pairs)} heads, worst rel-L2 O={worst[0]:.2e} dO={worst[1]:.2e} "
          f"LSE={worst[2]:.2e} fwd O={worst[3]:.2e} gQ={worst[4]:.2e} gK={worst[5]:.2e} gV={worst[6]:.2e} "
          f"Delta={worst[7]:.2e}")
+    del x, o, do, lse, of, lsef, gq, gk, gv, delta
+    torch.cuda.empty_cache()
     assert worst.max() <= TOL[dt], worst

@@ -360,9 +360,9 @@ def test_backward_entry_point_validates(lib):
 
 @_no_gpu
 def test_largest_accepted_sizes_pass_the_size_checks(lib):
-    # the largest bf16 head (L * D = 2^31), the largest fp32 head (L * D = 2^30) and an fp32
-    # forward of 2^20 (batch, head) pairs pass the size checks: the first failure is then a
-    # deliberately bad layout (checked later)
+    # the largest bf16 head (L * D = 2^31), the largest fp32 head (L * D = 2^30) and fp32
+    # launches over 2^20 (batch, head) pairs pass the size checks: the first failure is then
+    # a deliberately bad layout (checked later)
     bad = make_layout("teacher_forcing", [0, 16, 40])
     assert _call(lib, L=1 << 24, D=128, layout=bad) == 1 and "L = 2" in binding.last_error()
     assert _call(lib, dtype=0, L=1 << 23, D=128, layout=bad) == 1 and "L = 2" in binding.last_error()
@@ -370,11 +370,9 @@ def test_largest_accepted_sizes_pass_the_size_checks(lib):
     p = _ptrs(10, 2, 1, 1, 1 << 24, 128)
     rc = lib.attn_bwd(1, 1, 1, (1 << 24) + 2, 128, *p[:6], ctypes.byref(make_layout("full")), 0.0, *p[6:], None)
     assert rc == 1 and "2^31" in binding.last_error()
-    # the fp32 backward launches one grid row per (batch, head): at most 65535 of them
-    p = _ptrs(10, 4, 256, 256, 16, 64)
-    rc = lib.attn_bwd(0, 256, 256, 16, 64, *p[:6], ctypes.byref(bad), 0.0, *p[6:], None)
-    assert rc == 1 and "65535" in binding.last_error()
-    rc = lib.attn_bwd(0, 65535, 1, 16, 64, *p[:6], ctypes.byref(bad), 0.0, *p[6:], None)
+    # and so does an fp32 backward over 2^20 (batch, head) pairs
+    p = _ptrs(10, 4, 1024, 1024, 16, 64)
+    rc = lib.attn_bwd(0, 1024, 1024, 16, 64, *p[:6], ctypes.byref(bad), 0.0, *p[6:], None)
     assert rc == 1 and "L = 2" in binding.last_error()
 
 
