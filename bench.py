@@ -262,8 +262,20 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    def outputs():
+        if mode == "fwd":
+            return (o, lse)
+        if mode == "zc":
+            return (o, don, lse)
+        if mode == "bwd":
+            return (gq, gk, gv, delta)
+        return (o, do, lse)
+
     for _ in range(args.warmup):
         step()
+    torch.cuda.synchronize()
+    # outputs of the first launch (untimed copy), compared bit for bit with the last timed one
+    first = [t.clone() for t in outputs()] if args.warmup > 0 else None
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream(dev)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
@@ -274,6 +286,8 @@ def main():
         ev[i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    deterministic = None if first is None else all(torch.equal(a, b) for a, b in zip(first, outputs()))
+    del first
     per = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
     kernel_ms = ev[0].elapsed_time(ev[-1]) / args.steps
     ms_per_step = wall * 1e3 / args.steps
@@ -315,6 +329,8 @@ def main():
                       "min": round(min(per), 4)},
         "unmasked_pairs_per_head": pairs,
         "computed_over_unmasked": round(computed / pairs, 4),
+        # every output of the last timed launch equals the first launch's bit for bit
+        "deterministic": deterministic,
     }
     if prof.get("clock_ghz") and prof.get("trace_kernel_ms"):
         # The committed profile run of this kernel source (possibly on another box, whose shader

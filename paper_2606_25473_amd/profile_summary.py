@@ -26,6 +26,29 @@ OP_KERNEL = {"fwd": r"attn_mfma_kernel<\d+, 0, \d+>", "jvp": r"attn_mfma_kernel<
              "bwd_dq": r"attn_bwd_dq_kernel<\d+>"}
 
 
+# matrix-core flop per admissible (query, key) pair in each op's kernel (the zero-clean JVP's
+# varies with the pair's halves)
+OP_FLOP_PER_PAIR = {"fwd": 4, "jvp": 12, "zc": None, "bwd": 8, "bwd_dq": 6}
+
+
+def matrix_flop_line(op, workload, mflop):
+    """The counted matrix-core flop of one dispatch against the flop of the admissible pairs
+    (and, for the JVP, of the pairs its 256-row tile plans compute, masked lanes included)."""
+    from .binding import count_computed_pairs, count_unmasked_pairs
+    from .workloads import WORKLOADS
+    w = WORKLOADS[workload]
+    offs = list(w.offsets) or None
+    line = f"matrix-core flop (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512): {mflop:.4g} per dispatch"
+    f = OP_FLOP_PER_PAIR[op]
+    if f:
+        pairs = count_unmasked_pairs(w.kind, offs, w.L) * w.B * w.H
+        line += f" = {mflop / (pairs * f * w.D):.4f} x the {f} D flop of the admissible pairs"
+        if op == "jvp":
+            comp = count_computed_pairs(w.kind, offs, w.L, w.D) * w.B * w.H
+            line += f", {mflop / (comp * f * w.D):.4f} x that of the pairs the tile plans compute"
+    return line
+
+
 def attn_kernel_of(op):
     """Predicate on rocprofv3 kernel names selecting the bf16 kernel of ``op``."""
     pat = re.compile(OP_KERNEL[op])
@@ -129,6 +152,9 @@ def main(argv=None):
             derived["clock_ghz"] = cyc / statistics.median(dur)
             lines.append(f"shader clock during the kernel: {derived['clock_ghz']:.3f} GHz "
                          f"(GRBM_GUI_ACTIVE / {xcc} XCDs / dispatch time {statistics.median(dur) / 1e6:.3f} ms)")
+            if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in per:
+                mflop = statistics.median(per["SQ_INSTS_VALU_MFMA_MOPS_BF16"]) * 512
+                lines.append(matrix_flop_line(a.op, a.workload, mflop))
             if "SQ_VALU_MFMA_BUSY_CYCLES" in per:
                 simds = 1024
                 util = statistics.median(per["SQ_VALU_MFMA_BUSY_CYCLES"]) / (cyc * simds)

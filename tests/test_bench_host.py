@@ -123,3 +123,19 @@ def test_profile_summary_picks_the_kernel_of_the_op():
         pick = profile_summary.attn_kernel_of(op)
         assert pick(f"void attn::(anonymous namespace)::{name}(attn::AttnArgs)")
         assert not any(pick(n) for o, n in names.items() if o != op)
+
+
+def test_matrix_flop_line_compares_with_the_computed_pairs():
+    from paper_2606_25473_amd import count_computed_pairs, count_unmasked_pairs
+    from paper_2606_25473_amd.profile_summary import matrix_flop_line
+    from paper_2606_25473_amd.workloads import WORKLOADS
+    w = WORKLOADS["wan1.3b_chunkwise_tf"]
+    offs = list(w.offsets)
+    comp = count_computed_pairs(w.kind, offs, w.L, w.D) * w.B * w.H
+    pairs = count_unmasked_pairs(w.kind, offs, w.L) * w.B * w.H
+    line = matrix_flop_line("jvp", w.name, comp * 12 * w.D)
+    assert "1.0000 x that of the pairs the tile plans compute" in line
+    assert f"{comp / pairs:.4f} x the 12 D flop of the admissible pairs" in line
+    assert "admissible" in matrix_flop_line("bwd", w.name, pairs * 8 * w.D)
+    assert "x the" not in matrix_flop_line("zc", w.name, 1.0e13)
+
