@@ -227,6 +227,29 @@ def test_full_size_sampled_rows(name):
          f"dO={worst[1]:.3e} LSE={worst[2]:.3e}")
 
 
+def test_whole_head_bidirectional():
+    """One whole head of the Wan-shaped bidirectional workload (bf16, L = 32760, D = 128),
+    every row of O, dO and LSE (and of the forward's O and LSE) against the oracle."""
+    w = WORKLOADS["wan1.3b_bidirectional"]
+    b, h = 0, 5
+    _say(f"[whole head] {w.name} B={w.B} H={w.H} L={w.L}: generating inputs on the GPU")
+    x = make_inputs(w, "cuda", 0)
+    o, do, lse = attn_jvp_fwd(x["Q"], x["K"], x["V"], x["dQ"], x["dK"], x["dV"], w.kind, _offsets(w))
+    of, lsef = attn_fwd(x["Q"], x["K"], x["V"], w.kind, _offsets(w))
+    torch.cuda.synchronize()
+    _say(f"[whole head] kernels done; oracle over all {w.L} rows of head ({b}, {h})")
+    sl = {k: _np(v[b:b + 1, h:h + 1]) for k, v in x.items()}
+    O, dO, LSE = attention_jvp(sl["Q"], sl["K"], sl["V"], sl["dQ"], sl["dK"], sl["dV"], w.kind, _offsets(w))
+    errs = {"O": _rel(_np(o[b, h]), O[0, 0]), "dO": _rel(_np(do[b, h]), dO[0, 0]),
+            "LSE": _rel(_np(lse[b, h]), LSE[0, 0]), "fwd O": _rel(_np(of[b, h]), O[0, 0]),
+            "fwd LSE": _rel(_np(lsef[b, h]), LSE[0, 0])}
+    worst_row = float(np.max(np.linalg.norm(_np(do[b, h]) - dO[0, 0], axis=1) /
+                             np.maximum(np.linalg.norm(dO[0, 0], axis=1), 1e-300)))
+    _say(f"[whole head] rel-L2 " + " ".join(f"{n}={e:.3e}" for n, e in errs.items()) +
+         f"; worst single dO row {worst_row:.3e}")
+    assert max(errs.values()) <= TOL["bf16"], errs
+
+
 # ----------------------------------------------------------------------------- rescale stress
 
 def _scaled_inputs(w, seed, key_gain):
