@@ -76,6 +76,12 @@ SHAPES = [
     custom_workload("bwd_full_below_one_tile_bf16", 1, 1, 128, "bf16", MASK_FULL, L=7, tangent_std=0.5),
     custom_workload("bwd_full_single_token_bf16", 1, 1, 128, "bf16", MASK_FULL, L=1, tangent_std=0.5),
     custom_workload("bwd_full_d64_f32", 1, 2, 64, "f32", MASK_FULL, L=50),
+    custom_workload("bwd_tf_ragged_f32", 2, 2, 128, "f32", MASK_TEACHER_FORCING, 3, 100),
+    custom_workload("bwd_tf_several_tiles_f32", 1, 3, 64, "f32", MASK_TEACHER_FORCING, 4, 300),
+    custom_workload("bwd_tf_nonuniform_f32", 1, 2, 128, "f32", MASK_TEACHER_FORCING, offsets=[0, 1, 3, 7, 40, 41, 90, 200]),
+    custom_workload("bwd_block_causal_f32", 1, 2, 128, "f32", MASK_BLOCK_CAUSAL, offsets=[0, 50, 77, 200, 333]),
+    custom_workload("bwd_full_below_one_tile_f32", 1, 1, 128, "f32", MASK_FULL, L=7),
+    custom_workload("bwd_full_single_token_f32", 1, 1, 64, "f32", MASK_FULL, L=1),
     # rows 100..149 see no key; keys 450..499 are seen by no row
     custom_workload("bwd_ranges_bf16", 1, 2, 128, "bf16", MASK_RANGES,
                     offsets=[(0, 100, [(0, 100), (300, 350)]), (100, 150, []), (150, 400, [(0, 450)]),

@@ -81,6 +81,18 @@ EDGE = [
     custom_workload("tf_f32_d128", 1, 2, 128, "f32", MASK_TEACHER_FORCING, 3, 20),
     custom_workload("full_f32_d64", 1, 2, 64, "f32", MASK_FULL, L=50),
     custom_workload("block_causal_f32", 1, 1, 64, "f32", MASK_BLOCK_CAUSAL, offsets=[0, 3, 10, 31]),
+    # the fp32 kernels' own tiling (128-row tiles, 16 rows per wave, 32-key blocks): ragged
+    # tails, several tiles, a partial head group, one-token and single chunks, uneven offsets
+    custom_workload("tf_ragged_f32", 2, 2, 128, "f32", MASK_TEACHER_FORCING, 3, 100),
+    custom_workload("tf_several_tiles_f32", 1, 3, 128, "f32", MASK_TEACHER_FORCING, 4, 300),
+    custom_workload("tf_nine_heads_f32", 3, 3, 64, "f32", MASK_TEACHER_FORCING, 2, 170),
+    custom_workload("tf_one_token_chunks_f32", 1, 2, 128, "f32", MASK_TEACHER_FORCING, 64, 1),
+    custom_workload("tf_one_chunk_f32", 1, 2, 64, "f32", MASK_TEACHER_FORCING, 1, 300),
+    custom_workload("tf_nonuniform_f32", 1, 2, 128, "f32", MASK_TEACHER_FORCING, offsets=[0, 1, 3, 7, 40, 41, 90, 200]),
+    custom_workload("block_causal_uneven_f32", 1, 2, 128, "f32", MASK_BLOCK_CAUSAL, offsets=[0, 50, 77, 200, 333]),
+    custom_workload("full_1000_f32", 1, 2, 128, "f32", MASK_FULL, L=1000),
+    custom_workload("full_below_one_tile_f32", 1, 1, 128, "f32", MASK_FULL, L=7),
+    custom_workload("full_single_token_f32", 1, 1, 64, "f32", MASK_FULL, L=1),
 ]
 
 

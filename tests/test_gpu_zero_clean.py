@@ -70,6 +70,10 @@ SHAPES = [
     custom_workload("zc_d64_bf16", 1, 2, 64, "bf16", MASK_TEACHER_FORCING, 4, 50, tangent_std=0.5),
     custom_workload("zc_f32_d128", 1, 2, 128, "f32", MASK_TEACHER_FORCING, 3, 20),
     custom_workload("zc_f32_d64", 2, 1, 64, "f32", MASK_TEACHER_FORCING, offsets=[0, 5, 6, 30]),
+    # t0 = L/2 inside a 32-key block and a 128-row tile of the fp32 kernel, and on their bounds
+    custom_workload("zc_ragged_f32", 2, 2, 128, "f32", MASK_TEACHER_FORCING, 3, 100),
+    custom_workload("zc_tile_aligned_f32", 1, 2, 128, "f32", MASK_TEACHER_FORCING, 4, 128),
+    custom_workload("zc_nonuniform_f32", 1, 2, 64, "f32", MASK_TEACHER_FORCING, offsets=[0, 1, 3, 7, 40, 41, 90, 200]),
 ]
 
 
