@@ -1,4 +1,5 @@
-// attn_f32.hip -- fp32 masked attention forward + JVP on gfx950 matrix cores.
+// attn_f32.hip -- fp32 masked attention on gfx950 matrix cores: forward, JVP (dense and
+// with zero clean tangents) and the two backward passes (after the forward kernel below).
 //
 // The fp32 entry points keep every product and sum in fp32 (their bar is 1e-4 relative),
 // so this path uses fp32 matrix instructions: fp32 operands, fp32 accumulation.  The
