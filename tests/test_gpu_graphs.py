@@ -10,7 +10,9 @@ Checked here:
   replay equals the eager result bit for bit (the kernels are deterministic); after the
   inputs change in place, a replay follows the new inputs;
 * two JVP calls on two streams without synchronisation between them equal the same calls
-  made one after the other.
+  made one after the other;
+* the same for the fp32 kernels: every fp32 entry point in one graph, and an fp32 call
+  beside a bf16 call on two streams.
 """
 import sys
 
@@ -116,6 +118,55 @@ def test_two_streams_overlap():
     wb = custom_workload("streams_full", 2, 2, 128, "bf16", MASK_FULL, L=900, tangent_std=0.5)
     _say("[streams] two JVP calls on two streams")
     xa, xb = make_inputs(wa, "cuda", 24), make_inputs(wb, "cuda", 25)
+
+    def call(w, x, stream=None):
+        return attn_jvp_fwd(x["Q"], x["K"], x["V"], x["dQ"], x["dK"], x["dV"], w.kind,
+                            list(w.offsets) if w.offsets else None, stream=stream)
+
+    ra = [t.clone() for t in call(wa, xa)]
+    rb = [t.clone() for t in call(wb, xb)]
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    s1.wait_stream(torch.cuda.current_stream())
+    s2.wait_stream(torch.cuda.current_stream())
+    for _ in range(3):
+        with torch.cuda.stream(s1):
+            oa = call(wa, xa, s1)
+        with torch.cuda.stream(s2):
+            ob = call(wb, xb, s2)
+        torch.cuda.synchronize()
+        for a, b in zip(oa, ra):
+            assert torch.equal(a, b)
+        for a, b in zip(ob, rb):
+            assert torch.equal(a, b)
+
+
+def test_fp32_calls_in_a_graph():
+    w = custom_workload("graph_f32", 1, 2, 128, "f32", MASK_TEACHER_FORCING, 3, 150)
+    _say("[graph] fp32 attn_jvp_fwd, attn_jvp_fwd_zero_clean, attn_fwd and attn_bwd in one graph")
+    x = make_inputs(w, "cuda", 26)
+    half = w.L // 2
+    offs = list(w.offsets)
+    tn = {k: x[k][:, :, half:].contiguous() for k in ("dQ", "dK", "dV")}
+
+    def calls():
+        jvp = attn_jvp_fwd(x["Q"], x["K"], x["V"], x["dQ"], x["dK"], x["dV"], w.kind, offs)
+        zc = attn_jvp_fwd_zero_clean(x["Q"], x["K"], x["V"], tn["dQ"], tn["dK"], tn["dV"], offs)
+        o, lse = attn_fwd(x["Q"], x["K"], x["V"], w.kind, offs)
+        bwd = attn_bwd(x["Q"], x["K"], x["V"], o, x["dV"], lse, w.kind, offs)
+        return (*jvp, *zc, o, lse, *bwd)
+
+    eager = [t.clone() for t in calls()]
+    torch.cuda.synchronize()
+    g, out = _capture(calls)
+    _replays_equal(g, out, eager, x)
+
+
+def test_bf16_and_fp32_on_two_streams():
+    wa = custom_workload("streams_bf16", 1, 4, 128, "bf16", MASK_TEACHER_FORCING, 4, 300, tangent_std=0.5)
+    wb = custom_workload("streams_f32", 2, 2, 64, "f32", MASK_FULL, L=700)
+    _say("[streams] a bf16 and an fp32 JVP call on two streams")
+    xa, xb = make_inputs(wa, "cuda", 27), make_inputs(wb, "cuda", 28)
 
     def call(w, x, stream=None):
         return attn_jvp_fwd(x["Q"], x["K"], x["V"], x["dQ"], x["dK"], x["dV"], w.kind,
