@@ -29,6 +29,9 @@
  *   keeps no per-call state, so calls are reentrant and may be captured in a
  *   HIP graph.  Inputs are never written.  Outputs must not overlap inputs or
  *   each other (checked by address range; overlap is ATTN_ERR_INVALID).
+ * - Alignment: every [B, H, L, D] tensor pointer (inputs, tangents, O, dO, gO, gQ, gK,
+ *   gV) must be 16-byte aligned, LSE and Delta 4-byte aligned; otherwise
+ *   ATTN_ERR_INVALID.
  * - Sizes: B, H, L >= 1, B * H <= 2^20, ceil(L / 128) * B * H <= 2^31 - 1 (work-groups
  *   of one launch); the kernels address a head with 32-bit byte offsets, so bf16 inputs
  *   need L * D <= 2^31 and fp32 inputs L * D <= 2^30.  Larger sizes are

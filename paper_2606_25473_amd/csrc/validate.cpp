@@ -70,7 +70,7 @@ int prepare(Pass pass, int dtype, int B, int H, int L, int D, const void* Q, con
   const uintptr_t tbytes = (uintptr_t)B * H * L * D * es;
   const uintptr_t gbytes = (uintptr_t)B * H * (L - t0) * D * es;  // tangents and dO
   const uintptr_t lbytes = (uintptr_t)B * H * L * sizeof(float);
-  const uintptr_t align = dtype == ATTN_DTYPE_BF16 ? 16 : 4;
+  const uintptr_t align = 16;  // the kernels move tensor rows in 16-byte pieces
   const void* ins[6] = {Q, K, V, dQ, dK, dV};
   const char* in_names[6] = {"Q", "K", "V", "dQ", "dK", "dV"};
   const int nin = jvp ? 6 : 3;
@@ -136,7 +136,7 @@ int prepare_bwd(int dtype, int B, int H, int L, int D, const void* Q, const void
     if (!outs[i]) return fail(ATTN_ERR_INVALID, std::string("NULL pointer ") + out_names[i]);
   const uintptr_t tbytes = (uintptr_t)B * H * L * D * elem_size(dtype);
   const uintptr_t lbytes = (uintptr_t)B * H * L * sizeof(float);
-  const uintptr_t align = dtype == ATTN_DTYPE_BF16 ? 16 : 4;
+  const uintptr_t align = 16;  // the kernels move tensor rows in 16-byte pieces
   for (int i = 0; i < 6; ++i)
     if ((uintptr_t)ins[i] % (i < 5 ? align : 4))
       return fail(ATTN_ERR_INVALID, std::string(in_names[i]) + " is misaligned");

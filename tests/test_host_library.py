@@ -276,6 +276,9 @@ def _call(lib, **kw):
     (dict(ptrs=_with(0, 0)), 1, "NULL"),
     (dict(ptrs=_with(5, 0)), 1, "NULL"),
     (dict(ptrs=_with(0, FAKE + 2)), 1, "aligned"),
+    # fp32 tensors too are moved in 16-byte pieces: a 4-byte aligned Q or dV is refused
+    (dict(dtype=0, ptrs=_with(0, FAKE + 4)), 1, "16-byte aligned"),
+    (dict(dtype=0, ptrs=_with(5, FAKE + 5 * (64 * 64 * 4 + 4096) + 8)), 1, "16-byte aligned"),
     (dict(ptrs=_with(6, _ptrs()[0])), 1, "overlaps input"),
     (dict(ptrs=_with(7, _ptrs()[6] + 64)), 1, "overlap"),
     (dict(layout=make_layout("teacher_forcing", [0, 16, 40])), 1, "L = 2"),
@@ -354,6 +357,8 @@ def test_backward_entry_point_validates(lib):
     assert call(q) == 1 and "overlaps input Q" in binding.last_error()
     q = list(p); q[7] = q[6] + 1024
     assert call(q) == 1 and "overlap" in binding.last_error()
+    q = list(p); q[0] = q[0] + 4  # fp32 inputs need 16-byte alignment too
+    assert call(q, dtype=0) == 1 and "misaligned" in binding.last_error()
     assert call(p, D=80) == 2 and "head_dim" in binding.last_error()
     assert call(p, layout=make_layout("teacher_forcing", [0, 16, 40])) == 1 and "L = 2" in binding.last_error()
 
