@@ -117,6 +117,50 @@ def _check(w, q, k, v, go, o, lse, label):
     return gq, gk, gv, delta, ref
 
 
+def _random_groups(L, G, seed, max_ranges=5):
+    """Seeded query groups tiling [0, L), each with 0..max_ranges disjoint key ranges in
+    random order (some empty, some touching)."""
+    rng = np.random.default_rng(seed)
+    cuts = [0] + sorted(int(c) for c in rng.choice(np.arange(1, L), size=G - 1, replace=False)) + [L]
+    groups = []
+    for q0, q1 in zip(cuts, cuts[1:]):
+        n = int(rng.integers(0, max_ranges + 1))
+        pts = sorted(int(v) for v in rng.integers(0, L + 1, size=2 * n))
+        ks = [(pts[2 * i], pts[2 * i + 1]) for i in range(n)]
+        if n >= 2 and rng.random() < 0.3:
+            ks[1] = (ks[0][1], max(ks[0][1], ks[1][1]))
+        rng.shuffle(ks)
+        groups.append((q0, q1, [tuple(k) for k in ks]))
+    return groups
+
+
+def _striped_groups(L, G, stripes, width, seed):
+    """Groups of L/G rows, each admitting `stripes` narrow key ranges spread over the
+    sequence: more separate runs per key tile than a plan holds (merged and masked)."""
+    rng = np.random.default_rng(seed)
+    bounds = [round(i * L / G) for i in range(G + 1)]
+    return [(q0, q1, [(a, a + int(rng.integers(1, width + 1)))
+                      for a in sorted(int(v) for v in rng.choice(np.arange(0, L - width, 2 * width), size=stripes,
+                                                                   replace=False))])
+            for q0, q1 in zip(bounds, bounds[1:])]
+
+
+@pytest.mark.parametrize("dt,D,L,G,seed,stripes", [("bf16", 128, 700, 9, 31, 0), ("bf16", 64, 1500, 40, 32, 0),
+                                                   ("bf16", 128, 2100, 25, 35, 0), ("f32", 128, 300, 12, 33, 0),
+                                                   ("f32", 64, 500, 30, 34, 0), ("bf16", 128, 3000, 6, 36, 9),
+                                                   ("f32", 128, 900, 4, 37, 7)])
+def test_backward_random_range_lists(dt, D, L, G, seed, stripes):
+    """Seeded random range-list masks (fully masked groups, keys no row sees, touching and
+    unsorted ranges; or striped groups with more runs per tile than a plan holds)."""
+    groups = _striped_groups(L, G, stripes, 40, seed) if stripes else _random_groups(L, G, seed)
+    w = custom_workload(f"bwd_random_ranges_{dt}_{D}_{L}_{G}_{seed}", 1, 2, D, dt, MASK_RANGES, offsets=groups,
+                        tangent_std=0.5)
+    _say(f"[backward] {w.name} groups={groups[:2]}...")
+    q, k, v, go = _inputs(w, seed)
+    o, lse = _oracle_fwd(w, q, k, v)
+    _check(w, q, k, v, go, o, lse, "oracle O/LSE")
+
+
 @pytest.mark.parametrize("w", SHAPES, ids=[w.name for w in SHAPES])
 def test_backward_vs_oracle(w):
     _say(f"[backward] {w.name} B={w.B} H={w.H} L={w.L} D={w.D} {w.dtype} {w.kind}")
