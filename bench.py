@@ -34,7 +34,7 @@ sys.path.insert(0, ROOT)
 
 from paper_2606_25473_amd import (attn_bwd, attn_fwd, attn_jvp_fwd, attn_jvp_fwd_zero_clean,  # noqa: E402
                                   count_computed_pairs, count_unmasked_pairs, query_groups)
-from paper_2606_25473_amd.workloads import HEADLINE, WORKLOADS, make_inputs  # noqa: E402
+from paper_2606_25473_amd.workloads import HEADLINE, WORKLOADS, custom_workload, make_inputs  # noqa: E402
 
 METRIC = "masked attention fwd+JVP TFLOP/s (unmasked pairs) and % bf16 MFMA peak"
 # the line printed by the non-default modes names what they measure
@@ -50,14 +50,22 @@ PEAK_FP32_TFLOPS = 157.3
 KERNEL_SOURCES = ["paper_2606_25473_amd/csrc/attn_mfma.hip", "paper_2606_25473_amd/csrc/attn_bwd.hip",
                   "paper_2606_25473_amd/csrc/mfma_common.hpp", "paper_2606_25473_amd/csrc/schedule.hpp",
                   "paper_2606_25473_amd/csrc/kernels.hpp"]
+# the fp32 kernels' sources (their counter records are kept apart from the bf16 ones)
+KERNEL_SOURCES_F32 = ["paper_2606_25473_amd/csrc/attn_f32.hip", "paper_2606_25473_amd/csrc/mfma_common.hpp",
+                      "paper_2606_25473_amd/csrc/schedule.hpp", "paper_2606_25473_amd/csrc/kernels.hpp"]
 
 
-def kernel_source_hash():
+def kernel_source_hash(dtype="bf16"):
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in KERNEL_SOURCES if dtype == "bf16" else KERNEL_SOURCES_F32:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
+
+
+def record_key(workload, mode, dtype="bf16"):
+    """Key of a counter record in profiles/hbm_traffic.json."""
+    return f"{workload}:{mode}" if dtype == "bf16" else f"{workload}:{mode}:{dtype}"
 
 
 def zero_clean_flop(groups, half, D):
@@ -79,7 +87,7 @@ def zero_clean_flop(groups, half, D):
     return total
 
 
-def profile_record(workload, mode):
+def profile_record(workload, mode, dtype="bf16"):
     """The committed rocprofv3 counter record of this workload (HBM bytes per launch,
     shader clock, MFMA busy fraction), if it was taken on the current kernel source;
     else an empty dict."""
@@ -88,8 +96,8 @@ def profile_record(workload, mode):
         return {}
     with open(path) as f:
         rec = json.load(f)
-    ent = rec.get(f"{workload}:{mode}")
-    if not ent or ent.get("kernel_source_hash") != kernel_source_hash():
+    ent = rec.get(record_key(workload, mode, dtype))
+    if not ent or ent.get("kernel_source_hash") != kernel_source_hash(dtype):
         return {}
     return ent
 
@@ -198,6 +206,8 @@ def main():
     ap.add_argument("--zero-clean", action="store_true",
                     help="time attn_jvp_fwd_zero_clean (teacher forcing, zero clean-half tangents)")
     ap.add_argument("--backward", action="store_true", help="time attn_bwd (gradients for a cotangent of O)")
+    ap.add_argument("--dtype", choices=["bf16", "f32"],
+                    help="run the workload's shape with inputs of this dtype (default: the workload's)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -212,6 +222,9 @@ def main():
         sys.exit(1)
 
     w = WORKLOADS[args.workload]
+    if args.dtype and args.dtype != w.dtype:  # the same shape, mask and recipe in another dtype
+        w = custom_workload(w.name, w.B, w.H, w.D, args.dtype, w.kind, offsets=list(w.offsets) or None,
+                            L=w.L_full, tangent_std=w.tangent_std)
     if args.forward + args.zero_clean + args.backward > 1:
         ap.error("--forward, --zero-clean and --backward are exclusive")
     if args.zero_clean and w.kind != "teacher_forcing":
@@ -301,13 +314,13 @@ def main():
     value = flop / (ms_per_step * 1e-3) / 1e12
     achieved = flop / (kernel_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_TFLOPS
-    prof = profile_record(w.name, mode)
+    prof = profile_record(w.name, mode, w.dtype)
     traffic = prof.get("hbm_bytes_per_launch")
     if mode == "bwd" and traffic is not None:
         # a backward call is two launches; the record of the first (query-tile) pass is separate
-        traffic = traffic + profile_record(w.name, "bwd_dq").get("hbm_bytes_per_launch", float("nan"))
+        traffic = traffic + profile_record(w.name, "bwd_dq", w.dtype).get("hbm_bytes_per_launch", float("nan"))
     res = {
-        "metric": MODE_METRIC[mode],
+        "metric": MODE_METRIC[mode] if w.dtype == "bf16" else MODE_METRIC[mode].replace("bf16", "fp32"),
         "value": round(value, 3),
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -339,7 +352,7 @@ def main():
         # clock from that run's own launch time.
         clk, pms = prof["clock_ghz"], prof["trace_kernel_ms"]
         if mode == "bwd":  # a call is two launches: add the query-tile pass's time
-            pms += profile_record(w.name, "bwd_dq").get("trace_kernel_ms", float("nan"))
+            pms += profile_record(w.name, "bwd_dq", w.dtype).get("trace_kernel_ms", float("nan"))
         res["roofline"]["profile"] = {
             "kernel_ms": round(pms, 4), "clock_ghz": round(clk, 3),
             "frac_at_clock": round(flop / (pms * 1e-3) / 1e12 / (peak * clk / 2.4), 4),

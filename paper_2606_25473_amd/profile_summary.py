@@ -1,7 +1,8 @@
 """Summarise rocprofv3 CSV output of a bench.py run into a short text report.
 
     python -m paper_2606_25473_amd.profile_summary --trace DIR [--fetch DIR --write DIR]
-        [--copy-mib N] [--workload NAME] [--op jvp|fwd|zc|bwd|bwd_dq] [--record profiles/hbm_traffic.json]
+        [--copy-mib N] [--workload NAME] [--op jvp|fwd|zc|bwd|bwd_dq] [--dtype bf16|f32]
+        [--record profiles/hbm_traffic.json]
 
 --trace: a ``rocprofv3 --kernel-trace --stats -f csv`` output directory;
 --fetch/--write: ``rocprofv3 --pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE`` output
@@ -24,6 +25,10 @@ import statistics
 OP_KERNEL = {"fwd": r"attn_mfma_kernel<\d+, 0, \d+>", "jvp": r"attn_mfma_kernel<\d+, 1, \d+>",
              "zc": r"attn_mfma_kernel<\d+, 2, \d+>", "bwd": r"attn_bwd_dkdv_kernel<\d+>",
              "bwd_dq": r"attn_bwd_dq_kernel<\d+>"}
+# the fp32 kernels (one kernel serves the dense and the zero-clean JVP)
+OP_KERNEL_F32 = {"fwd": r"attn_f32_kernel<\d+, false>", "jvp": r"attn_f32_kernel<\d+, true>",
+                 "zc": r"attn_f32_kernel<\d+, true>", "bwd": r"attn_f32_bwd_dkdv_kernel<\d+>",
+                 "bwd_dq": r"attn_f32_bwd_dq_kernel<\d+>"}
 
 
 # matrix-core flop per admissible (query, key) pair in each op's kernel (the zero-clean JVP's
@@ -31,27 +36,33 @@ OP_KERNEL = {"fwd": r"attn_mfma_kernel<\d+, 0, \d+>", "jvp": r"attn_mfma_kernel<
 OP_FLOP_PER_PAIR = {"fwd": 4, "jvp": 12, "zc": None, "bwd": 8, "bwd_dq": 6}
 
 
-def matrix_flop_line(op, workload, mflop):
+def matrix_flop_line(op, workload, mflop, dtype="bf16"):
     """The counted matrix-core flop of one dispatch against the flop of the admissible pairs
-    (and, for the JVP, of the pairs its 256-row tile plans compute, masked lanes included)."""
+    (and, for the bf16 JVP, of the pairs its 256-row tile plans compute, masked lanes
+    included)."""
     from .binding import count_computed_pairs, count_unmasked_pairs
     from .workloads import WORKLOADS
     w = WORKLOADS[workload]
     offs = list(w.offsets) or None
-    line = f"matrix-core flop (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512): {mflop:.4g} per dispatch"
+    line = f"matrix-core flop ({mops_counter(dtype)} x 512): {mflop:.4g} per dispatch"
     f = OP_FLOP_PER_PAIR[op]
     if f:
         pairs = count_unmasked_pairs(w.kind, offs, w.L) * w.B * w.H
         line += f" = {mflop / (pairs * f * w.D):.4f} x the {f} D flop of the admissible pairs"
-        if op == "jvp":
+        if op == "jvp" and dtype == "bf16":
             comp = count_computed_pairs(w.kind, offs, w.L, w.D) * w.B * w.H
             line += f", {mflop / (comp * f * w.D):.4f} x that of the pairs the tile plans compute"
     return line
 
 
-def attn_kernel_of(op):
-    """Predicate on rocprofv3 kernel names selecting the bf16 kernel of ``op``."""
-    pat = re.compile(OP_KERNEL[op])
+def mops_counter(dtype):
+    """The counter of matrix-core operations (512 flop each) of the dtype's kernels."""
+    return "SQ_INSTS_VALU_MFMA_MOPS_BF16" if dtype == "bf16" else "SQ_INSTS_VALU_MFMA_MOPS_F32"
+
+
+def attn_kernel_of(op, dtype="bf16"):
+    """Predicate on rocprofv3 kernel names selecting the kernel of ``op`` for ``dtype``."""
+    pat = re.compile((OP_KERNEL if dtype == "bf16" else OP_KERNEL_F32)[op])
     return lambda name: bool(pat.search(name))
 
 
@@ -95,6 +106,7 @@ def main(argv=None):
     ap.add_argument("--copy-mib", type=int, default=0)
     ap.add_argument("--workload", default="wan1.3b_chunkwise_tf")
     ap.add_argument("--op", default="jvp", choices=sorted(OP_KERNEL))
+    ap.add_argument("--dtype", default="bf16", choices=["bf16", "f32"])
     ap.add_argument("--record")
     ap.add_argument("--pmc", nargs="*", default=[], help="counter-collection output dirs to list")
     a = ap.parse_args(argv)
@@ -102,7 +114,7 @@ def main(argv=None):
     derived = {}
     if a.trace:
         st = sorted(kernel_stats(a.trace), key=lambda r: -r[2] * r[1])
-        mine = [r for r in st if attn_kernel_of(a.op)(r[0])]
+        mine = [r for r in st if attn_kernel_of(a.op, a.dtype)(r[0])]
         if mine:
             derived["trace_kernel_ms"] = mine[0][2] / 1e6  # mean launch time under the tracer
         lines.append("| kernel | calls | avg ms | min ms | max ms | % time |")
@@ -117,7 +129,7 @@ def main(argv=None):
             per = counter_per_dispatch(d, cnt)
             # the calibration copy is a device-to-device hipMemcpy (runtime blit kernel)
             cname, cvals = _pick(per, "copyBuffer")
-            kname, kvals = _pick(per, attn_kernel_of(a.op))
+            kname, kvals = _pick(per, attn_kernel_of(a.op, a.dtype))
             if not cvals or not kvals:
                 lines.append(f"{cnt}: copy or attention kernel missing in {d}")
                 continue
@@ -132,7 +144,7 @@ def main(argv=None):
             traffic = out["read"] + out["write"]
             lines.append(f"HBM traffic per launch: {traffic / 1e9:.3f} GB "
                          f"(read {out['read'] / 1e9:.3f} + write {out['write'] / 1e9:.3f})")
-    is_attn = attn_kernel_of(a.op)
+    is_attn = attn_kernel_of(a.op, a.dtype)
     for d in a.pmc:
         per, dur = {}, []
         for r in _rows(d, "counter_collection.csv"):
@@ -152,9 +164,9 @@ def main(argv=None):
             derived["clock_ghz"] = cyc / statistics.median(dur)
             lines.append(f"shader clock during the kernel: {derived['clock_ghz']:.3f} GHz "
                          f"(GRBM_GUI_ACTIVE / {xcc} XCDs / dispatch time {statistics.median(dur) / 1e6:.3f} ms)")
-            if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in per:
-                mflop = statistics.median(per["SQ_INSTS_VALU_MFMA_MOPS_BF16"]) * 512
-                lines.append(matrix_flop_line(a.op, a.workload, mflop))
+            if mops_counter(a.dtype) in per:
+                mflop = statistics.median(per[mops_counter(a.dtype)]) * 512
+                lines.append(matrix_flop_line(a.op, a.workload, mflop, a.dtype))
             if "SQ_VALU_MFMA_BUSY_CYCLES" in per:
                 simds = 1024
                 util = statistics.median(per["SQ_VALU_MFMA_BUSY_CYCLES"]) / (cyc * simds)
@@ -172,9 +184,9 @@ def main(argv=None):
         if os.path.exists(a.record):
             with open(a.record) as f:
                 rec = json.load(f)
-        ent = {"hbm_bytes_per_launch": traffic, "kernel_source_hash": bench.kernel_source_hash()}
+        ent = {"hbm_bytes_per_launch": traffic, "kernel_source_hash": bench.kernel_source_hash(a.dtype)}
         ent.update(derived)
-        rec[f"{a.workload}:{a.op}"] = ent
+        rec[bench.record_key(a.workload, a.op, a.dtype)] = ent
         with open(a.record, "w") as f:
             json.dump(rec, f, indent=1, sort_keys=True)
 

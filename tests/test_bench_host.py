@@ -68,18 +68,25 @@ def test_more_than_one_gpu_is_refused():
 def test_counter_record_of_other_sources_is_ignored(tmp_path, monkeypatch):
     (tmp_path / "profiles").mkdir()
     rec = {"w:jvp": {"hbm_bytes_per_launch": 123.0, "kernel_source_hash": "current"},
-           "w:fwd": {"hbm_bytes_per_launch": 456.0, "kernel_source_hash": "older"}}
+           "w:fwd": {"hbm_bytes_per_launch": 456.0, "kernel_source_hash": "older"},
+           "w:bwd:f32": {"hbm_bytes_per_launch": 789.0, "kernel_source_hash": "current"}}
     (tmp_path / "profiles" / "hbm_traffic.json").write_text(json.dumps(rec))
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
-    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "current")
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda dtype="bf16": "current")
     assert bench.profile_record("w", "jvp")["hbm_bytes_per_launch"] == 123.0
     assert bench.profile_record("w", "fwd") == {}
     assert bench.profile_record("w", "zc") == {}
+    # fp32 records sit under their own keys
+    assert bench.profile_record("w", "bwd", "f32")["hbm_bytes_per_launch"] == 789.0
+    assert bench.profile_record("w", "bwd") == {} and bench.profile_record("w", "jvp", "f32") == {}
 
 
 def test_kernel_source_hash_covers_the_kernel_sources():
-    assert all(os.path.exists(os.path.join(ROOT, p)) for p in bench.KERNEL_SOURCES)
+    assert all(os.path.exists(os.path.join(ROOT, p)) for p in bench.KERNEL_SOURCES + bench.KERNEL_SOURCES_F32)
     assert len(bench.kernel_source_hash()) == 16
+    # the bf16 and fp32 records depend on different sources and are kept apart
+    assert bench.kernel_source_hash("f32") != bench.kernel_source_hash("bf16")
+    assert bench.record_key("w", "jvp") == "w:jvp" and bench.record_key("w", "jvp", "f32") == "w:jvp:f32"
 
 
 def _counter_csv(path, rows):
@@ -123,6 +130,14 @@ def test_profile_summary_picks_the_kernel_of_the_op():
         pick = profile_summary.attn_kernel_of(op)
         assert pick(f"void attn::(anonymous namespace)::{name}(attn::AttnArgs)")
         assert not any(pick(n) for o, n in names.items() if o != op)
+    f32 = {"fwd": "attn_f32_kernel<128, false>", "jvp": "attn_f32_kernel<64, true>",
+           "bwd": "attn_f32_bwd_dkdv_kernel<128>", "bwd_dq": "attn_f32_bwd_dq_kernel<64>"}
+    for op, name in f32.items():
+        pick = profile_summary.attn_kernel_of(op, "f32")
+        assert pick(f"void attn::(anonymous namespace)::{name}(attn::AttnArgs)")
+        assert not any(pick(n) for o, n in f32.items() if o != op)
+        assert not any(pick(n) for n in names.values())
+    assert profile_summary.attn_kernel_of("zc", "f32")("attn_f32_kernel<128, true>(attn::AttnArgs)")
 
 
 def test_matrix_flop_line_compares_with_the_computed_pairs():
