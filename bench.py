@@ -341,9 +341,9 @@ def main():
         "kernel_ms": {"mean": round(kernel_ms, 4), "median": round(float(np.median(per)), 4),
                       "min": round(min(per), 4)},
         "unmasked_pairs_per_head": pairs,
-        # pairs the bf16 kernels' 256-row tile plans evaluate, masked lanes included (the fp32
-        # kernels tile by 128 rows: not reported for them)
-        "computed_over_unmasked": round(computed / pairs, 4) if w.dtype == "bf16" else None,
+        # pairs the bf16 JVP kernel's 256-row tile plans evaluate, masked lanes included (the
+        # other kernels tile differently: not reported for them)
+        "computed_over_unmasked": round(computed / pairs, 4) if w.dtype == "bf16" and mode == "jvp" else None,
         # every output of the last timed launch equals the first launch's bit for bit
         "deterministic": deterministic,
     }
