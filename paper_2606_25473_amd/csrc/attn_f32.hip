@@ -48,6 +48,8 @@ constexpr int BC = 32;       // keys per block
 constexpr int NW = 8;        // waves per work-group (two per SIMD)
 constexpr int QW = 16;       // query rows per wave
 constexpr int BR = QW * NW;  // query rows per work-group
+// the host sizes the grids and tile orders with these
+static_assert(BR == kF32Br && BR == kBwdKeysPerTile, "fp32 tiles must match the host's tile sizes");
 constexpr float kLazyF = 8.0f;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
